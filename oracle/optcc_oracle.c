@@ -1,0 +1,434 @@
+/*
+ * OptCC oracle: plain serial CPU reference of the schedule-driven
+ * reduce-and-forward data movement.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may include, link,
+ * load or call this file.  It shares no code, header, table or constant with
+ * the GPU library; both are written independently from the paper and from the
+ * readings listed with the design notes.
+ *
+ * Source of every rule below (paper: "Don't Let a Few Network Failures Slow
+ * the Entire AllReduce"):
+ *   - problem setting, slowdown factor l = 1/b, correctness = every rank ends
+ *     with the elementwise sum .......................... Sec. 3 (problem setting)
+ *   - k segments of p-1 sections of s = n/(k(p-1)) ........ Sec. 4.1
+ *   - Stage 1 reduce-scatter chain on the healthy ring, Stage 2 upload,
+ *     Stage 3 download, Stage 4 allgather ................. Sec. 4.1 (Stages 1-4)
+ *   - the two valid stage orderings (1) S1-S2-S3-S4 and
+ *     (2) S3-S1-S4-S2 ...................................... Sec. 4.1 (stage ordering)
+ *   - patterns A/C (ordering 1), B/D (ordering 2), k/4
+ *     segments per pattern ................................. Sec. 4.2 (four patterns, pipelining)
+ *   - bubble filling for l < 2: per segment p-1 sections of s' and one
+ *     point-to-point allreduce chunk of D = (2-l)s'/l, with
+ *     s' = n l / (k((p-2)l+2)) ............................ Sec. 4.2 (bubble filling), App. C
+ *   - m >= 2 stragglers: p-m sections of s = n/(k(p-m)),
+ *     patterns B, D, A', C' ................................ App. D
+ *
+ * Step model.  One step writes one destination range of one rank:
+ *   COPY   : dst <- src
+ *   REDUCE : acc = widen(dst); acc = acc + widen(src_i) for each source in
+ *            listed order; dst <- narrow(acc)
+ * widen/narrow are the identity for fp32 and int32 (int32 adds wrap modulo
+ * 2^32); for bf16, widen is the exact 16-bit shift to fp32 and narrow rounds
+ * fp32 to bf16 to nearest, ties to even.  Every step rounds once, so a chain
+ * of hops rounds at every hop, as a bf16 wire would.
+ *
+ * Steps carry a slot number 0..5 that orders the stages of every section:
+ *   0 straggler raw values folded into the chain start (ordering 2's Stage 3,
+ *     and the non-finalising stragglers of A'/C')
+ *   1 Stage 1 chain            2 Stage 2 upload (ordering 1) / P2P up
+ *   3 Stage 3 download (ordering 1) / P2P down
+ *   4 Stage 4 allgather        5 G sent to the remaining stragglers
+ *                                (ordering 2's Stage 2, A'/C' non-finalisers)
+ * Running all steps of slot 0, then slot 1, ... is one valid serial order:
+ * segments never share coordinates, and within a section the slot order is
+ * the section's own stage order.
+ *
+ * Build:  gcc -O2 -std=c99 -ffp-contract=off -fno-fast-math -shared -fPIC
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_F32 0
+#define ORC_BF16 1
+#define ORC_I32 2
+
+#define ORC_COPY 0
+#define ORC_REDUCE 1
+
+/* Plan kinds. */
+#define ORC_RING 0       /* no straggler: textbook ring */
+#define ORC_SINGLE_GE2 1 /* one straggler, l >= 2 */
+#define ORC_SINGLE_LT2 2 /* one straggler, 1 < l < 2: bubble filling */
+#define ORC_MULTI 3      /* m >= 2 stragglers */
+
+/* Split quantum in elements: every section and P2P chunk is a whole number
+ * of quanta (the last quantum of the vector may be partial). */
+#define ORC_QUANTUM 64
+
+typedef struct {
+  int32_t slot, seg, sec, op, dst, nsrc;
+  int64_t src_at; /* index into the source pool */
+  int64_t off, len;
+} orc_step;
+
+typedef struct {
+  int p, k, m, kind, pp; /* pp = P' = number of healthy ranks */
+  int64_t n;
+  double ell[1024];      /* l_i = max_b / b_i */
+  int ring[1024];        /* healthy ranks, ascending */
+  int strag[1024];       /* stragglers sorted by l descending, ties lower rank */
+  int seg_lo, seg_hi;    /* segments whose steps were built */
+  /* per-segment split (all k segments) */
+  int64_t *seg_off, *seg_len, *p2p_len;
+  int64_t nsteps, cap_steps, nsrcpool, cap_srcpool;
+  orc_step *steps;
+  int32_t *srcpool;
+} orc_sched;
+
+static const char *g_err = "";
+const char *orc_last_error(void) { return g_err; }
+
+/* ---------------------------------------------------------------- steps */
+
+static int push_step(orc_sched *s, int slot, int seg, int sec, int op, int dst,
+                     const int *srcs, int nsrc, int64_t off, int64_t len) {
+  if (len <= 0) return 0; /* an empty section moves nothing */
+  if (s->nsteps == s->cap_steps) {
+    int64_t nc = s->cap_steps ? 2 * s->cap_steps : 1024;
+    orc_step *ns = (orc_step *)realloc(s->steps, (size_t)nc * sizeof(orc_step));
+    if (!ns) return -2;
+    s->steps = ns;
+    s->cap_steps = nc;
+  }
+  while (s->nsrcpool + nsrc > s->cap_srcpool) {
+    int64_t nc = s->cap_srcpool ? 2 * s->cap_srcpool : 4096;
+    int32_t *np = (int32_t *)realloc(s->srcpool, (size_t)nc * sizeof(int32_t));
+    if (!np) return -2;
+    s->srcpool = np;
+    s->cap_srcpool = nc;
+  }
+  orc_step *st = &s->steps[s->nsteps++];
+  st->slot = slot;
+  st->seg = seg;
+  st->sec = sec;
+  st->op = op;
+  st->dst = dst;
+  st->nsrc = nsrc;
+  st->src_at = s->nsrcpool;
+  st->off = off;
+  st->len = len;
+  for (int i = 0; i < nsrc; ++i) s->srcpool[s->nsrcpool++] = srcs[i];
+  return 0;
+}
+
+/* Healthy-ring position arithmetic: R[(j + t) mod P']. */
+static int ring_at(const orc_sched *s, int j, int t) {
+  int pp = s->pp;
+  int idx = ((j + t) % pp + pp) % pp;
+  return s->ring[idx];
+}
+
+/* The steps of one ring section j of segment g, covering [off, off+len).
+ * ordering: 1 = S1-S2-S3-S4, 2 = S3-S1-S4-S2 (Sec. 4.1).  For m >= 2 the
+ * ordering-1 segments (A', C') let the worst straggler finalise and fold the
+ * others in at the chain start, the exact reading of App. D. */
+static int section_steps(orc_sched *s, int g, int j, int ordering, int64_t off,
+                         int64_t len) {
+  int pp = s->pp, m = s->m, rc = 0;
+  int holder = ring_at(s, j, pp - 1); /* R[j-1]: where Stage 1 ends */
+  int one[1];
+  int *pre = (int *)malloc(sizeof(int) * (size_t)(m > 0 ? m : 1));
+  if (!pre) return -2;
+
+  /* slot 0: stragglers' raw values join at the chain start R[j]. */
+  int npre = 0;
+  if (m >= 1 && ordering == 2)
+    for (int i = 0; i < m; ++i) pre[npre++] = s->strag[i];
+  if (m >= 2 && ordering == 1)
+    for (int i = 1; i < m; ++i) pre[npre++] = s->strag[i];
+  if (npre > 0) rc |= push_step(s, 0, g, j, ORC_REDUCE, ring_at(s, j, 0), pre, npre, off, len);
+
+  /* slot 1, Stage 1: P'-1 hops; the receiver adds its own value. */
+  for (int t = 1; t <= pp - 1; ++t) {
+    one[0] = ring_at(s, j, t - 1);
+    rc |= push_step(s, 1, g, j, ORC_REDUCE, ring_at(s, j, t), one, 1, off, len);
+  }
+
+  if (m >= 1 && ordering == 1) {
+    int fin = s->strag[0];
+    /* slot 2, Stage 2: the holder uploads its partial; the straggler adds its
+     * own value and so holds the global sum. */
+    one[0] = holder;
+    rc |= push_step(s, 2, g, j, ORC_REDUCE, fin, one, 1, off, len);
+    /* slot 3, Stage 3: the global sum goes back to the holder. */
+    one[0] = fin;
+    rc |= push_step(s, 3, g, j, ORC_COPY, holder, one, 1, off, len);
+  }
+
+  /* slot 4, Stage 4: allgather from the holder along the ring. */
+  for (int t = 0; t <= pp - 2; ++t) {
+    one[0] = ring_at(s, j, t - 1);
+    rc |= push_step(s, 4, g, j, ORC_COPY, ring_at(s, j, t), one, 1, off, len);
+  }
+
+  /* slot 5: the global sum reaches the stragglers that did not finalise. */
+  if (m >= 1) {
+    int first = (ordering == 1) ? 1 : 0;
+    for (int i = first; i < m; ++i) {
+      one[0] = holder;
+      rc |= push_step(s, 5, g, j, ORC_COPY, s->strag[i], one, 1, off, len);
+    }
+  }
+  free(pre);
+  return rc;
+}
+
+/* The point-to-point allreduce chunk of a segment (bubble filling, Sec. 4.2):
+ * every healthy rank sends its own chunk to the straggler, which sums its own
+ * value first and then R[0..P'-1] in ring order; the sum is broadcast back. */
+static int p2p_steps(orc_sched *s, int g, int64_t off, int64_t len) {
+  int rc = 0, one[1];
+  int st = s->strag[0];
+  rc |= push_step(s, 2, g, -1, ORC_REDUCE, st, s->ring, s->pp, off, len);
+  for (int i = 0; i < s->pp; ++i) {
+    one[0] = st;
+    rc |= push_step(s, 3, g, -1, ORC_COPY, s->ring[i], one, 1, off, len);
+  }
+  return rc;
+}
+
+/* ------------------------------------------------------------- building */
+
+void orc_free(orc_sched *s) {
+  if (!s) return;
+  free(s->steps);
+  free(s->srcpool);
+  free(s->seg_off);
+  free(s->seg_len);
+  free(s->p2p_len);
+  free(s);
+}
+
+/* Build the schedule for segments [seg_lo, seg_hi) (all segments when
+ * seg_hi <= 0).  Returns 0, or a negative status with orc_last_error set. */
+int orc_build(int p, const double *bw, int64_t n, int k, int seg_lo, int seg_hi,
+              orc_sched **out) {
+  *out = NULL;
+  if (p < 3 || p > 1024) { g_err = "p must be in [3, 1024]"; return -1; }
+  if (n < 0) { g_err = "N must be >= 0"; return -1; }
+  if (k < 4 || k % 4 != 0) { g_err = "n_chunks must be a positive multiple of 4"; return -1; }
+  double bmax = 0.0;
+  for (int i = 0; i < p; ++i) {
+    if (!(bw[i] > 0.0) || !isfinite(bw[i])) { g_err = "bandwidths must be finite and > 0"; return -1; }
+    if (bw[i] > bmax) bmax = bw[i];
+  }
+  orc_sched *s = (orc_sched *)calloc(1, sizeof(orc_sched));
+  if (!s) return -2;
+  s->p = p;
+  s->n = n;
+  s->k = k;
+  for (int i = 0; i < p; ++i) s->ell[i] = bmax / bw[i];
+
+  /* Stragglers: ranks slower than the fastest, by l descending, then rank. */
+  int m = 0, pp = 0;
+  for (int i = 0; i < p; ++i) {
+    if (bw[i] < bmax) s->strag[m++] = i;
+    else s->ring[pp++] = i;
+  }
+  for (int a = 1; a < m; ++a) { /* insertion sort, stable on rank */
+    int v = s->strag[a], b = a - 1;
+    while (b >= 0 && s->ell[s->strag[b]] < s->ell[v]) { s->strag[b + 1] = s->strag[b]; --b; }
+    s->strag[b + 1] = v;
+  }
+  s->m = m;
+  s->pp = pp;
+  if (pp < 2) { orc_free(s); g_err = "fewer than 2 healthy ranks"; return -3; }
+  if (m == 0) s->kind = ORC_RING;
+  else if (m == 1) s->kind = (s->ell[s->strag[0]] >= 2.0) ? ORC_SINGLE_GE2 : ORC_SINGLE_LT2;
+  else s->kind = ORC_MULTI;
+
+  /* Segment split: NQ quanta, segment g owns quanta [g NQ / k, (g+1) NQ / k). */
+  s->seg_off = (int64_t *)calloc((size_t)k, sizeof(int64_t));
+  s->seg_len = (int64_t *)calloc((size_t)k, sizeof(int64_t));
+  s->p2p_len = (int64_t *)calloc((size_t)k, sizeof(int64_t));
+  if (!s->seg_off || !s->seg_len || !s->p2p_len) { orc_free(s); return -2; }
+  int64_t nq = (n + ORC_QUANTUM - 1) / ORC_QUANTUM;
+  if (seg_hi <= 0 || seg_hi > k) seg_hi = k;
+  if (seg_lo < 0) seg_lo = 0;
+  s->seg_lo = seg_lo;
+  s->seg_hi = seg_hi;
+
+  for (int g = 0; g < k; ++g) {
+    int64_t q0 = (int64_t)g * nq / k, q1 = (int64_t)(g + 1) * nq / k;
+    int64_t lq = q1 - q0;
+    /* Bubble filling: the P2P chunk holds D/L = (2-l)/((p-2)l+2) of the
+     * segment, rounded to whole quanta (App. C data accounting). */
+    int64_t dq = 0;
+    if (s->kind == ORC_SINGLE_LT2) {
+      double l = s->ell[s->strag[0]];
+      double x = ((double)lq * (2.0 - l)) / ((double)(p - 2) * l + 2.0);
+      dq = (int64_t)floor(x + 0.5);
+      if (dq < 0) dq = 0;
+      if (dq > lq) dq = lq;
+    }
+    int64_t rq = lq - dq; /* quanta on the ring path */
+    int64_t qb = rq / pp, big = rq % pp;
+    int64_t seg_b = q0 * ORC_QUANTUM < n ? q0 * ORC_QUANTUM : n;
+    int64_t seg_e = q1 * ORC_QUANTUM < n ? q1 * ORC_QUANTUM : n;
+    s->seg_off[g] = seg_b;
+    s->seg_len[g] = seg_e - seg_b;
+    int64_t pb = (q1 - dq) * ORC_QUANTUM, pe = q1 * ORC_QUANTUM;
+    if (pb > n) pb = n;
+    if (pe > n) pe = n;
+    s->p2p_len[g] = pe - pb;
+    if (g < seg_lo || g >= seg_hi) continue;
+
+    /* Pattern of segment g: A,B,C,D for one straggler, B,D,A',C' for several;
+     * A, C, A', C' use ordering 1 and B, D use ordering 2. */
+    int pat = g % 4, ordering;
+    if (m <= 1) ordering = (pat == 0 || pat == 2) ? 1 : 2;
+    else ordering = (pat <= 1) ? 2 : 1;
+
+    int64_t qcur = q0;
+    for (int j = 0; j < pp; ++j) {
+      int64_t ql = qb + (j < big ? 1 : 0);
+      int64_t b = qcur * ORC_QUANTUM, e = (qcur + ql) * ORC_QUANTUM;
+      if (b > n) b = n;
+      if (e > n) e = n;
+      if (section_steps(s, g, j, ordering, b, e - b)) { orc_free(s); g_err = "out of memory"; return -2; }
+      qcur += ql;
+    }
+    if (dq > 0 && p2p_steps(s, g, pb, pe - pb)) { orc_free(s); g_err = "out of memory"; return -2; }
+  }
+
+  /* Serial order: by slot, keeping build order (segment, section, hop)
+   * within a slot.  Counting sort over the six slots keeps it stable. */
+  int64_t cnt[7] = {0};
+  for (int64_t i = 0; i < s->nsteps; ++i) cnt[s->steps[i].slot + 1]++;
+  for (int q = 0; q < 6; ++q) cnt[q + 1] += cnt[q];
+  orc_step *sorted = (orc_step *)malloc((size_t)(s->nsteps ? s->nsteps : 1) * sizeof(orc_step));
+  if (!sorted) { orc_free(s); return -2; }
+  for (int64_t i = 0; i < s->nsteps; ++i) sorted[cnt[s->steps[i].slot]++] = s->steps[i];
+  free(s->steps);
+  s->steps = sorted;
+  s->cap_steps = s->nsteps;
+  *out = s;
+  return 0;
+}
+
+/* ------------------------------------------------------------ accessors */
+
+int orc_info(const orc_sched *s, int64_t *out8, int *ring, int *strag, double *ell) {
+  out8[0] = s->p; out8[1] = s->k; out8[2] = s->m; out8[3] = s->kind;
+  out8[4] = s->pp; out8[5] = s->n; out8[6] = s->nsteps; out8[7] = s->nsrcpool;
+  for (int i = 0; i < s->pp; ++i) ring[i] = s->ring[i];
+  for (int i = 0; i < s->m; ++i) strag[i] = s->strag[i];
+  for (int i = 0; i < s->p; ++i) ell[i] = s->ell[i];
+  return 0;
+}
+
+void orc_segments(const orc_sched *s, int64_t *off, int64_t *len, int64_t *p2p) {
+  for (int g = 0; g < s->k; ++g) { off[g] = s->seg_off[g]; len[g] = s->seg_len[g]; p2p[g] = s->p2p_len[g]; }
+}
+
+/* Export the steps as parallel arrays: ints[i*6 + .] = slot, seg, sec, op,
+ * dst, nsrc; offs[i*3 + .] = src_at, off, len; pool = source ranks. */
+void orc_steps(const orc_sched *s, int32_t *ints, int64_t *offs, int32_t *pool) {
+  for (int64_t i = 0; i < s->nsteps; ++i) {
+    const orc_step *st = &s->steps[i];
+    int32_t *a = ints + 6 * i;
+    a[0] = st->slot; a[1] = st->seg; a[2] = st->sec; a[3] = st->op; a[4] = st->dst; a[5] = st->nsrc;
+    int64_t *b = offs + 3 * i;
+    b[0] = st->src_at; b[1] = st->off; b[2] = st->len;
+  }
+  memcpy(pool, s->srcpool, (size_t)s->nsrcpool * sizeof(int32_t));
+}
+
+/* ------------------------------------------------------------ arithmetic */
+
+static float bf16_widen(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* fp32 -> bf16, round to nearest, ties to even (NaN stays NaN, quietened). */
+static uint16_t bf16_narrow(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+  uint32_t lsb = (u >> 16) & 1u;
+  u += 0x7fffu + lsb;
+  return (uint16_t)(u >> 16);
+}
+
+uint16_t orc_bf16_round(float f) { return bf16_narrow(f); }
+
+void orc_bf16_round_array(const float *x, uint16_t *y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) y[i] = bf16_narrow(x[i]);
+}
+
+/* One step applied to element c of every involved buffer. */
+static void apply_elem(int dtype, const orc_step *st, const int32_t *srcs, void **bufs,
+                       int64_t c) {
+  if (dtype == ORC_F32) {
+    float **b = (float **)bufs;
+    if (st->op == ORC_COPY) { b[st->dst][c] = b[srcs[0]][c]; return; }
+    float acc = b[st->dst][c];
+    for (int i = 0; i < st->nsrc; ++i) acc = acc + b[srcs[i]][c];
+    b[st->dst][c] = acc;
+  } else if (dtype == ORC_BF16) {
+    uint16_t **b = (uint16_t **)bufs;
+    if (st->op == ORC_COPY) { b[st->dst][c] = b[srcs[0]][c]; return; }
+    float acc = bf16_widen(b[st->dst][c]);
+    for (int i = 0; i < st->nsrc; ++i) acc = acc + bf16_widen(b[srcs[i]][c]);
+    b[st->dst][c] = bf16_narrow(acc);
+  } else {
+    uint32_t **b = (uint32_t **)bufs;
+    if (st->op == ORC_COPY) { b[st->dst][c] = b[srcs[0]][c]; return; }
+    uint32_t acc = b[st->dst][c];
+    for (int i = 0; i < st->nsrc; ++i) acc = acc + b[srcs[i]][c];
+    b[st->dst][c] = acc;
+  }
+}
+
+/* Execute every step with slot in [slot_lo, slot_hi), serially, in order,
+ * over whole rank buffers (p host pointers of N elements). */
+int orc_run(const orc_sched *s, int dtype, void **bufs, int slot_lo, int slot_hi) {
+  if (dtype < 0 || dtype > 2) { g_err = "bad dtype"; return -1; }
+  for (int64_t i = 0; i < s->nsteps; ++i) {
+    const orc_step *st = &s->steps[i];
+    if (st->slot < slot_lo || st->slot >= slot_hi) continue;
+    const int32_t *srcs = s->srcpool + st->src_at;
+    for (int64_t c = st->off; c < st->off + st->len; ++c) apply_elem(dtype, st, srcs, bufs, c);
+  }
+  return 0;
+}
+
+/* Same as orc_run restricted to the sorted coordinates coords[0..S): cols
+ * holds p host pointers to S values each (column i of rank r is coordinate
+ * coords[i]).  Used to check full-size runs at sampled coordinates. */
+int orc_run_sampled(const orc_sched *s, int dtype, void **cols, const int64_t *coords,
+                    int64_t S, int slot_lo, int slot_hi) {
+  if (dtype < 0 || dtype > 2) { g_err = "bad dtype"; return -1; }
+  for (int64_t i = 1; i < S; ++i)
+    if (coords[i] <= coords[i - 1]) { g_err = "coords must be strictly increasing"; return -1; }
+  for (int64_t i = 0; i < s->nsteps; ++i) {
+    const orc_step *st = &s->steps[i];
+    if (st->slot < slot_lo || st->slot >= slot_hi) continue;
+    const int32_t *srcs = s->srcpool + st->src_at;
+    /* first sampled coordinate >= st->off */
+    int64_t lo = 0, hi = S;
+    while (lo < hi) {
+      int64_t mid = lo + (hi - lo) / 2;
+      if (coords[mid] < st->off) lo = mid + 1; else hi = mid;
+    }
+    for (int64_t a = lo; a < S && coords[a] < st->off + st->len; ++a)
+      apply_elem(dtype, st, srcs, cols, a);
+  }
+  return 0;
+}
