@@ -1,0 +1,200 @@
+/*
+ * optcc.h - C ABI of the OptCC schedule-execution library for MI355X (gfx950).
+ *
+ * OptCC ("Don't Let a Few Network Failures Slow the Entire AllReduce") is a
+ * four-stage pipelined AllReduce for clusters in which a few ranks' NICs are
+ * slower (stragglers).  This library builds its schedule and executes every
+ * step of it on one GPU, where the p logical ranks are p buffers in HBM:
+ * after optcc_allreduce_emulate every buffer holds the elementwise sum of all
+ * p inputs (Sec. 3, problem setting: correctness conditions (i) and (ii)).
+ *
+ * Conventions for every entry point:
+ *   - status codes: OPTCC_OK (0) or a negative OPTCC_E* value; the message of
+ *     the last failure on the calling thread is returned by optcc_last_error.
+ *   - the library never aborts and never allocates on behalf of the caller
+ *     except where stated.
+ *   - device memory (bufs) is caller-owned.  A plan is host memory owned by
+ *     the caller (optcc_plan / optcc_plan_free); it lazily owns one small
+ *     read-only device copy of its step tables per device it has run on.
+ *   - "stream" is a hipStream_t (NULL = the default stream).  Emulation calls
+ *     are asynchronous and return once the kernels are enqueued.
+ */
+#ifndef OPTCC_H
+#define OPTCC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OPTCC_OK 0
+#define OPTCC_EINVAL (-1)      /* bad argument, or arguments that disagree with the plan */
+#define OPTCC_ENOMEM (-2)      /* host or device allocation failed */
+#define OPTCC_EUNSUPPORTED (-3) /* outside the method's domain (p < 3, fewer than 2 healthy ranks) or this build's limits */
+#define OPTCC_EDEVICE (-4)     /* a HIP runtime call failed; the message names it */
+
+#define OPTCC_MAX_RANKS 1024        /* largest p a plan accepts */
+#define OPTCC_MAX_EMULATE_RANKS 256 /* largest p the GPU executor accepts */
+#define OPTCC_NUM_SLOTS 6           /* stage slots, see optcc_allreduce_emulate_slots */
+#define OPTCC_QUANTUM 64            /* split quantum in elements */
+
+typedef struct optcc_plan optcc_plan_t;
+
+typedef enum { OPTCC_F32 = 0, OPTCC_BF16 = 1, OPTCC_I32 = 2 } optcc_dtype_t;
+
+typedef enum {
+  OPTCC_KIND_RING = 0,       /* no straggler: the ring of Sec. 3 (T0) */
+  OPTCC_KIND_SINGLE_GE2 = 1, /* one straggler with l >= 2 (Sec. 4.3, first case) */
+  OPTCC_KIND_SINGLE_LT2 = 2, /* one straggler with l < 2: bubble filling (Sec. 4.2, App. C) */
+  OPTCC_KIND_MULTI = 3       /* m >= 2 stragglers (App. D) */
+} optcc_kind_t;
+
+/*
+ * optcc_plan - build the OptCC schedule for p ranks (Sec. 4.1-4.2, App. C, App. D).
+ *
+ *   p               number of ranks, 3 <= p <= OPTCC_MAX_RANKS (Sec. 3 needs p >= 3)
+ *   link_bandwidths host array of p finite values > 0, any unit.  Slowdowns
+ *                   are l_i = max(b) / b_i; every rank slower than the fastest
+ *                   is a straggler, sorted by l descending, ties to lower rank.
+ *   N               elements per rank, N >= 0
+ *   n_chunks        k, the number of segments: a positive multiple of 4
+ *                   (Sec. 4.2: k/4 segments per pattern)
+ *   out             receives the plan; untouched on failure
+ *
+ * Split: quanta of OPTCC_QUANTUM elements; segment g owns quanta
+ * [floor(g*NQ/k), floor((g+1)*NQ/k)) with NQ = ceil(N/64).  For one straggler
+ * with l < 2 each segment ends with a point-to-point chunk of
+ * floor(Lq*(2-l)/((p-2)*l+2) + 0.5) quanta (App. C: D = (2-l)s'/l); the rest
+ * is split over the P' = p - m healthy ranks' sections, the first (rem)
+ * sections one quantum larger.  Ranges are clipped at N.
+ * Errors: OPTCC_EINVAL (bad p/N/k/bandwidths), OPTCC_EUNSUPPORTED (p > limit,
+ * fewer than 2 healthy ranks), OPTCC_ENOMEM.  No device call is made.
+ */
+int optcc_plan(int p, const double *link_bandwidths, int64_t N, int n_chunks,
+               optcc_plan_t **out);
+
+/* Free a plan and its device tables.  The caller guarantees that no emulation
+ * using it is still running on any stream.  NULL is ignored. */
+void optcc_plan_free(optcc_plan_t *plan);
+
+/*
+ * optcc_allreduce_emulate - execute every step of the plan, in place, as one
+ * fused launch on `stream` (Sec. 4.1 Stages 1-4 for every section in its
+ * pattern's stage ordering, plus App. C bubble filling and App. D's
+ * stragglers).  On completion every buffer holds the elementwise sum.
+ *
+ *   bufs   host array of p device pointers; bufs[r] holds rank r's N elements
+ *          of `dtype`, aligned to the element size.  Buffers must not overlap.
+ *          16-byte alignment of every pointer enables the vector path.
+ *   p, N   must equal the plan's
+ *   dtype  OPTCC_F32 (fp32 adds), OPTCC_BF16 (fp32 accumulation, one
+ *          round-to-nearest-even per step), OPTCC_I32 (adds modulo 2^32)
+ *
+ * Every step writes its destination rank's buffer; a partial sum that the
+ * next step of the same section consumes is kept in registers.  The result is
+ * bitwise deterministic.  Errors: OPTCC_EINVAL (mismatch with the plan, NULL
+ * or misaligned pointers, overlapping buffers), OPTCC_EUNSUPPORTED
+ * (p > OPTCC_MAX_EMULATE_RANKS), OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the
+ * plan on a device allocates its tables).
+ */
+int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
+                            const optcc_plan_t *plan, void *stream);
+
+/*
+ * optcc_allreduce_emulate_slots - execute only the steps whose stage slot is
+ * in [slot_begin, slot_end), either fused in one launch (launches = 1) or as
+ * one launch per slot (launches = 0), same buffers and errors as above.
+ * Slots (each section uses a subset, always in increasing order):
+ *   0  stragglers' raw values folded into the chain start (ordering 2, Sec. 4.1;
+ *      the non-finalising stragglers of A'/C', App. D)
+ *   1  Stage 1 reduce-scatter chain        2  Stage 2 upload; P2P up (App. C)
+ *   3  Stage 3 download; P2P down          4  Stage 4 allgather
+ *   5  global sum to the stragglers that did not finalise (ordering 2 Stage 2)
+ * After [0, s) the buffers equal the state after the first s slots of every
+ * section; [0, 6) is the whole AllReduce.
+ */
+int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
+                                  const optcc_plan_t *plan, int slot_begin, int slot_end,
+                                  int launches, void *stream);
+
+/*
+ * optcc_model_time - completion time of the plan's schedule in the paper's
+ * bandwidth-bound model (a healthy NIC moves one element per time unit; Sec. 3),
+ * for N elements per rank, in fp64:
+ *   no straggler      T0 = 2(p-1)N/p
+ *   one, l >= 2       l N (k+1)/k                                   (Sec. 4.3)
+ *   one, l < 2        2(p-1) l N/((p-2)l+2) * (k+l-1)/k             (Sec. 4.3, App. C)
+ *   m >= 2            (k+4) max{2(p-1)s, (l_1(p-m)+2(m-1))s}, s = N/(k(p-m))  (App. D)
+ * link_bandwidths may be NULL (use the plan's) or must give the same
+ * stragglers and slowdowns (relative difference <= 1e-12).  Returns NaN on
+ * error, with optcc_last_error set.
+ */
+double optcc_model_time(const optcc_plan_t *plan, const double *link_bandwidths);
+
+/*
+ * optcc_lower_bound - best known lower bound on any correct AllReduce for
+ * this profile and N, in the same unit (App. A, best lower bounds):
+ *   no straggler  T0;  one straggler  max{2l(p-1)/(l(p-2)+2), l} N  (tight bound, App. B.1);
+ *   m >= 2        max{2(p-1)/(p-m+sum 1/l_i), l_1} N  (Theorem 2).
+ * Returns NaN on invalid input (p < 3, bad bandwidths, N < 0).
+ */
+double optcc_lower_bound(int p, const double *link_bandwidths, int64_t N);
+
+/* Message of the last failure on the calling thread ("" if none). */
+const char *optcc_last_error(void);
+
+/* ------------------------------------------------------------ introspection
+ * Plan data for tests and reports.  No code is shared with any checker. */
+
+typedef struct {
+  int32_t p, k, m, kind;
+  int32_t healthy;  /* P' = p - m */
+  int32_t quantum;  /* OPTCC_QUANTUM */
+  int64_t n;
+  int64_t num_steps; /* steps: one destination write each */
+  int64_t num_flows; /* flows: one per (step, source rank) */
+} optcc_plan_info_t;
+
+/* Fill info and, when non-NULL, ring[P'] (healthy ranks in ring order),
+ * stragglers[m] (sorted) and slowdowns[p]. */
+int optcc_plan_info(const optcc_plan_t *plan, optcc_plan_info_t *info, int32_t *ring,
+                    int32_t *stragglers, double *slowdowns);
+
+/* Per segment (k entries each): element offset, length, and length of the
+ * trailing point-to-point chunk (0 unless bubble filling). */
+int optcc_plan_segments(const optcc_plan_t *plan, int64_t *offset, int64_t *length,
+                        int64_t *p2p_length);
+
+typedef struct {
+  int32_t slot;    /* 0..5, see optcc_allreduce_emulate_slots */
+  int32_t segment; /* 0..k-1 */
+  int32_t section; /* 0..P'-1, or -1 for the point-to-point chunk */
+  int32_t op;      /* 0 copy, 1 reduce (dst += src) */
+  int32_t src, dst;
+  int64_t step;    /* index of the step: the sources of a multi-source reduce
+                      share it and are listed in accumulation order */
+  int64_t offset, length; /* element range */
+} optcc_flow_t;
+
+/* Number of flows, and the flows in execution order (slot, segment, section,
+ * hop).  get_flows writes min(cap, total) entries and returns the total, or a
+ * negative status. */
+int64_t optcc_plan_num_flows(const optcc_plan_t *plan);
+int64_t optcc_plan_get_flows(const optcc_plan_t *plan, optcc_flow_t *out, int64_t cap);
+
+/*
+ * Algorithmic HBM bytes of one emulation call over [slot_begin, slot_end)
+ * with `launches` as above: every load the executor must issue (each input
+ * value once, plus the state a launch starts from) and every step's
+ * destination write.  Writes: optcc counts each step write once.
+ */
+int optcc_plan_traffic(const optcc_plan_t *plan, optcc_dtype_t dtype, int slot_begin,
+                       int slot_end, int launches, int64_t *read_bytes,
+                       int64_t *write_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPTCC_H */

@@ -1,0 +1,417 @@
+// GPU executor of the OptCC schedule on one MI355X (gfx950, CDNA4).
+//
+// The p logical ranks are p buffers in HBM.  One workgroup takes one tile of
+// 2048 consecutive elements of one segment's ring sections (or of its
+// point-to-point chunk) and runs, lane by lane, every step of the schedule
+// that touches those elements, in the section's own stage order: the
+// partial sum a hop forwards stays in registers, and every step still writes
+// its destination rank's buffer.  All arithmetic is elementwise, so the work
+// is a streaming reduction bound by HBM bandwidth; no matrix cores are used.
+//
+// Stage slots per section (paper: "Don't Let a Few Network Failures Slow the
+// Entire AllReduce", Sec. 4.1 Stages 1-4 and the two stage orderings,
+// Sec. 4.2 patterns and bubble filling, App. C, App. D):
+//   0 straggler raw values folded into the chain start R[j]
+//   1 Stage 1 reduce-scatter chain R[j] -> R[j+1] -> ... -> R[j-1] (holder)
+//   2 Stage 2: the finalising straggler adds the holder's partial;
+//     P2P up: the straggler sums its own chunk and every healthy rank's
+//   3 Stage 3: the global sum returns to the holder; P2P down
+//   4 Stage 4 allgather holder -> R[j] -> ... -> R[j+P'-2]
+//   5 the global sum reaches the stragglers that did not finalise
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "optcc_internal.hpp"
+
+namespace optcc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxRanks = OPTCC_MAX_EMULATE_RANKS;
+constexpr int kHopBatch = 8;  // loads in flight per vector along a chain
+
+struct KArgs {
+  const TileDesc *tiles;
+  const SegDesc *segs;
+  int64_t ntiles;
+  int64_t n;
+  int32_t pp, m;
+  int32_t sb, se;  // slot range [sb, se)
+  // rank pointers: [0, pp) healthy ranks in ring order, [pp, pp+m) stragglers
+  // sorted by slowdown (worst first)
+  void *ptr[kMaxRanks];
+};
+
+// ----------------------------------------------------------- element types
+// widen / narrow / add of one element; a step is narrow(widen(a) + widen(b)).
+struct F32 {
+  using S = float;
+  using A = float;
+  __device__ static A widen(S x) { return x; }
+  __device__ static S narrow(A x) { return x; }
+};
+struct I32 {
+  using S = uint32_t;  // two's complement adds wrap modulo 2^32
+  using A = uint32_t;
+  __device__ static A widen(S x) { return x; }
+  __device__ static S narrow(A x) { return x; }
+};
+struct BF16 {
+  using S = uint16_t;
+  using A = float;
+  __device__ static A widen(S x) { return __uint_as_float((uint32_t)x << 16); }
+  // round to nearest, ties to even; NaN stays NaN
+  __device__ static S narrow(A f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (S)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (S)(u >> 16);
+  }
+};
+
+template <class D, int W>
+struct alignas(sizeof(typename D::S) * W) Vec {
+  typename D::S v[W];
+};
+
+template <class D, int W>
+__device__ __forceinline__ Vec<D, W> vload(const void *base, int64_t e) {
+  return *reinterpret_cast<const Vec<D, W> *>(static_cast<const typename D::S *>(base) + e);
+}
+template <class D, int W>
+__device__ __forceinline__ void vstore(void *base, int64_t e, const Vec<D, W> &x) {
+  *reinterpret_cast<Vec<D, W> *>(static_cast<typename D::S *>(base) + e) = x;
+}
+// One reduce step with a single source: narrow(widen(a) + widen(b)).
+template <class D, int W>
+__device__ __forceinline__ Vec<D, W> add2(const Vec<D, W> &a, const Vec<D, W> &b) {
+  Vec<D, W> r;
+#pragma unroll
+  for (int i = 0; i < W; ++i) r.v[i] = D::narrow(D::widen(a.v[i]) + D::widen(b.v[i]));
+  return r;
+}
+template <class D, int W>
+struct AccV {
+  typename D::A v[W];
+};
+template <class D, int W>
+__device__ __forceinline__ AccV<D, W> widen(const Vec<D, W> &a) {
+  AccV<D, W> r;
+#pragma unroll
+  for (int i = 0; i < W; ++i) r.v[i] = D::widen(a.v[i]);
+  return r;
+}
+template <class D, int W>
+__device__ __forceinline__ void accum(AccV<D, W> &acc, const Vec<D, W> &b) {
+#pragma unroll
+  for (int i = 0; i < W; ++i) acc.v[i] = acc.v[i] + D::widen(b.v[i]);
+}
+template <class D, int W>
+__device__ __forceinline__ Vec<D, W> narrow(const AccV<D, W> &a) {
+  Vec<D, W> r;
+#pragma unroll
+  for (int i = 0; i < W; ++i) r.v[i] = D::narrow(a.v[i]);
+  return r;
+}
+
+__device__ __forceinline__ bool in_range(const KArgs &a, int q) { return a.sb <= q && q < a.se; }
+
+// ------------------------------------------------------- one ring section
+// Every step of section j (segment descriptor sd) for the W elements at e.
+// rp[i] is the i-th healthy rank's buffer in ring order (LDS copy).
+template <class D, int W>
+__device__ void ring_lane(const KArgs &a, void *const *rp, const SegDesc &sd, int j, int64_t e) {
+  using V = Vec<D, W>;
+  const int pp = a.pp, m = a.m;
+  const int ord = sd.ordering;
+  const int nside = m == 0 ? 0 : (ord == 2 ? m : m - 1);
+  const int sfirst = ord == 2 ? 0 : 1;
+  const bool fin = m >= 1 && ord == 1;  // a straggler finalises in Stages 2/3
+  auto pos = [&](int t) {               // ring position of R[j + t], 0 <= t < 2 pp
+    int i = j + t;
+    return i >= pp ? i - pp : i;
+  };
+  void *const holder = rp[pos(pp - 1)];
+  V v;
+  bool have = false;
+
+  // Stage 2's straggler operand does not depend on the chain: load it early.
+  V xs;
+  const bool do2 = fin && in_range(a, 2);
+  if (do2) xs = vload<D, W>(a.ptr[pp], e);
+
+  if (in_range(a, 0) && nside > 0) {  // slot 0
+    AccV<D, W> acc = widen(vload<D, W>(rp[j], e));
+    for (int i = 0; i < nside; ++i) accum(acc, vload<D, W>(a.ptr[pp + sfirst + i], e));
+    v = narrow(acc);
+    vstore<D, W>(rp[j], e, v);
+    have = true;
+  }
+  if (in_range(a, 1)) {  // slot 1: Stage 1 chain, loads kHopBatch hops ahead
+    if (!have) v = vload<D, W>(rp[j], e);
+    const int nh = pp - 1;
+    V cur[kHopBatch], nxt[kHopBatch];
+#pragma unroll
+    for (int u = 0; u < kHopBatch; ++u)
+      if (u < nh) cur[u] = vload<D, W>(rp[pos(1 + u)], e);
+    for (int t = 0; t < nh; t += kHopBatch) {
+#pragma unroll
+      for (int u = 0; u < kHopBatch; ++u)
+        if (t + kHopBatch + u < nh) nxt[u] = vload<D, W>(rp[pos(1 + t + kHopBatch + u)], e);
+#pragma unroll
+      for (int u = 0; u < kHopBatch; ++u)
+        if (t + u < nh) {
+          v = add2<D, W>(cur[u], v);
+          vstore<D, W>(rp[pos(1 + t + u)], e, v);
+        }
+#pragma unroll
+      for (int u = 0; u < kHopBatch; ++u) cur[u] = nxt[u];
+    }
+    have = true;
+  }
+  if (fin) {
+    if (do2) {  // slot 2: straggler <- straggler + holder's partial
+      if (!have) v = vload<D, W>(holder, e);
+      v = add2<D, W>(xs, v);
+      vstore<D, W>(a.ptr[pp], e, v);
+      have = true;
+    }
+    if (in_range(a, 3)) {  // slot 3: holder <- global sum
+      if (!have) v = vload<D, W>(a.ptr[pp], e);
+      vstore<D, W>(holder, e, v);
+      have = true;
+    }
+  }
+  if (in_range(a, 4)) {  // slot 4: allgather
+    if (!have) v = vload<D, W>(holder, e);
+    for (int t = 0; t + 1 < pp; ++t) vstore<D, W>(rp[pos(t)], e, v);
+    have = true;
+  }
+  if (in_range(a, 5) && nside > 0) {  // slot 5
+    if (!have) v = vload<D, W>(holder, e);
+    for (int i = 0; i < nside; ++i) vstore<D, W>(a.ptr[pp + sfirst + i], e, v);
+  }
+}
+
+// ------------------------------------------------- one point-to-point chunk
+// Bubble filling (Sec. 4.2, App. C): the straggler sums its own value and
+// R[0..P'-1] in that order, rounding once, and broadcasts the result.
+template <class D, int W>
+__device__ void p2p_lane(const KArgs &a, void *const *rp, int64_t e) {
+  using V = Vec<D, W>;
+  const int pp = a.pp;
+  V g;
+  bool have = false;
+  if (in_range(a, 2)) {
+    AccV<D, W> acc = widen(vload<D, W>(a.ptr[pp], e));
+    for (int t = 0; t < pp; t += kHopBatch) {
+      V x[kHopBatch];
+#pragma unroll
+      for (int u = 0; u < kHopBatch; ++u)
+        if (t + u < pp) x[u] = vload<D, W>(rp[t + u], e);
+#pragma unroll
+      for (int u = 0; u < kHopBatch; ++u)
+        if (t + u < pp) accum(acc, x[u]);
+    }
+    g = narrow(acc);
+    vstore<D, W>(a.ptr[pp], e, g);
+    have = true;
+  }
+  if (in_range(a, 3)) {
+    if (!have) g = vload<D, W>(a.ptr[pp], e);
+    for (int i = 0; i < pp; ++i) vstore<D, W>(rp[i], e, g);
+  }
+}
+
+// Section index of the quantum u of a segment's ring part.
+__device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
+  const uint32_t u = (uint32_t)u64;  // quanta within one segment fit in 32 bits
+  const uint32_t big = (uint32_t)sd.nbig * (uint32_t)(sd.qbase + 1);
+  if (u < big) return (int)(u / (uint32_t)(sd.qbase + 1));
+  return sd.nbig + (int)((u - big) / (uint32_t)sd.qbase);
+}
+
+template <class D, int W>
+__device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const SegDesc &sd,
+                                          bool p2p, int64_t e) {
+  if (p2p) {
+    p2p_lane<D, W>(a, rp, e);
+  } else {
+    const int j = section_of(sd, (e - sd.ring_begin) / kQuantum);
+    ring_lane<D, W>(a, rp, sd, j, e);
+  }
+}
+
+// W elements per lane access: 16 bytes when every rank buffer is 16-byte
+// aligned, else 1 element.  Elements of a tile past a whole vector (only at
+// the end of the rank vectors) go one by one.
+template <class D, int W>
+__global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
+  __shared__ void *rp[kMaxRanks];
+  for (int i = threadIdx.x; i < a.pp; i += kThreads) rp[i] = a.ptr[i];
+  __syncthreads();
+  for (int64_t t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    const TileDesc td = a.tiles[t];
+    const bool p2p = td.meta & 1;
+    const SegDesc sd = a.segs[td.meta >> 1];
+    const int64_t end = td.begin + td.len;
+    for (int64_t e = td.begin + (int64_t)threadIdx.x * W; e < end; e += (int64_t)kThreads * W) {
+      if (e + W <= end) {
+        run_elems<D, W>(a, rp, sd, p2p, e);
+      } else {
+        for (int64_t x = e; x < end; ++x) run_elems<D, 1>(a, rp, sd, p2p, x);
+      }
+    }
+  }
+}
+
+template <class D>
+hipError_t launch(const KArgs &a, bool vec16, hipStream_t st) {
+  constexpr int W16 = 16 / (int)sizeof(typename D::S);
+  const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
+  const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
+  if (vec16) hipLaunchKernelGGL((optcc_exec_kernel<D, W16>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((optcc_exec_kernel<D, 1>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return fail(OPTCC_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(err));
+  std::lock_guard<std::mutex> lk(pl.mu);
+  auto it = pl.dev.find(dev);
+  if (it != pl.dev.end()) {
+    *out = it->second;
+    return OPTCC_OK;
+  }
+  // Tiles: 2048-element pieces of every segment's ring part and P2P chunk.
+  std::vector<TileDesc> tiles;
+  for (int g = 0; g < pl.k; ++g) {
+    const Segment &s = pl.seg[(size_t)g];
+    auto cut = [&](int64_t b, int64_t e, int is_p2p) {
+      for (int64_t x = b; x < e; x += kTileElems) {
+        TileDesc t;
+        t.begin = x;
+        t.len = (int32_t)std::min<int64_t>(kTileElems, e - x);
+        t.meta = (g << 1) | is_p2p;
+        tiles.push_back(t);
+      }
+    };
+    cut(std::min(s.ring_begin, pl.n), s.ring_end, 0);
+    cut(s.p2p_begin, s.p2p_end, 1);
+  }
+  DeviceTables d;
+  const size_t sb = pl.segdesc.size() * sizeof(SegDesc), tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
+  err = hipMalloc(&d.segs, sb);
+  if (err == hipSuccess) err = hipMalloc(&d.tiles, tb);
+  if (err == hipSuccess) err = hipMemcpy(d.segs, pl.segdesc.data(), sb, hipMemcpyHostToDevice);
+  if (err == hipSuccess && !tiles.empty())
+    err = hipMemcpy(d.tiles, tiles.data(), tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice);
+  if (err != hipSuccess) {
+    if (d.segs) (void)hipFree(d.segs);
+    if (d.tiles) (void)hipFree(d.tiles);
+    return fail(err == hipErrorOutOfMemory ? OPTCC_ENOMEM : OPTCC_EDEVICE,
+                std::string("uploading plan tables: ") + hipGetErrorString(err));
+  }
+  d.ntiles = (int64_t)tiles.size();
+  pl.dev[dev] = d;
+  *out = d;
+  return OPTCC_OK;
+}
+
+int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optcc_plan_t *pl,
+            int sb, int se, int launches, void *stream) {
+  set_error("");
+  if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
+  if (!bufs) return fail(OPTCC_EINVAL, "bufs is NULL");
+  if (p != pl->p || N != pl->n) return fail(OPTCC_EINVAL, "p or N differ from the plan's");
+  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
+    return fail(OPTCC_EINVAL, "unknown dtype");
+  if (sb < 0 || se > OPTCC_NUM_SLOTS || sb > se) return fail(OPTCC_EINVAL, "slot range must satisfy 0 <= begin <= end <= 6");
+  if (launches != 0 && launches != 1) return fail(OPTCC_EINVAL, "launches must be 0 (one per slot) or 1 (fused)");
+  if (p > kMaxRanks) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_EMULATE_RANKS");
+  const size_t es = dtype == OPTCC_BF16 ? 2 : 4;
+  // pointers: non-NULL, element-aligned, pairwise disjoint
+  std::vector<std::pair<uintptr_t, int>> ranges;
+  bool vec16 = true;
+  for (int r = 0; r < p; ++r) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(bufs[r]);
+    if (!a) return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is NULL");
+    if (a % es) return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is not aligned to the element size");
+    if (a % 16) vec16 = false;
+    ranges.push_back({a, r});
+  }
+  std::sort(ranges.begin(), ranges.end());
+  for (size_t i = 1; i < ranges.size() && N > 0; ++i)
+    if (ranges[i - 1].first + (uintptr_t)N * es > ranges[i].first)
+      return fail(OPTCC_EINVAL, "rank buffers overlap");
+  if (N == 0 || sb == se) return OPTCC_OK;
+
+  DeviceTables dt;
+  int rc = device_tables(*pl, &dt);
+  if (rc != OPTCC_OK) return rc;
+  KArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.tiles = dt.tiles;
+  a.segs = dt.segs;
+  a.ntiles = dt.ntiles;
+  a.n = N;
+  a.pp = pl->pp;
+  a.m = pl->m;
+  for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
+  for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int nl = launches == 1 ? 1 : se - sb;
+  for (int l = 0; l < nl; ++l) {
+    a.sb = launches == 1 ? sb : sb + l;
+    a.se = launches == 1 ? se : sb + l + 1;
+    hipError_t err = hipSuccess;
+    switch (dtype) {
+      case OPTCC_F32: err = launch<F32>(a, vec16, st); break;
+      case OPTCC_BF16: err = launch<BF16>(a, vec16, st); break;
+      default: err = launch<I32>(a, vec16, st); break;
+    }
+    if (err != hipSuccess)
+      return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));
+  }
+  return OPTCC_OK;
+}
+
+}  // namespace
+}  // namespace optcc
+
+using namespace optcc;
+
+extern "C" int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
+                                       const optcc_plan_t *plan, void *stream) {
+  return emulate(bufs, p, N, dtype, plan, 0, OPTCC_NUM_SLOTS, 1, stream);
+}
+
+extern "C" int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N,
+                                             optcc_dtype_t dtype, const optcc_plan_t *plan,
+                                             int slot_begin, int slot_end, int launches,
+                                             void *stream) {
+  return emulate(bufs, p, N, dtype, plan, slot_begin, slot_end, launches, stream);
+}
+
+extern "C" void optcc_plan_free(optcc_plan_t *pl) {
+  if (!pl) return;
+  if (!pl->dev.empty()) {
+    std::lock_guard<std::mutex> lk(pl->mu);
+    int cur = -1;
+    const bool have_dev = hipGetDevice(&cur) == hipSuccess;
+    for (auto &kv : pl->dev) {
+      if (have_dev) (void)hipSetDevice(kv.first);
+      (void)hipFree(kv.second.segs);
+      (void)hipFree(kv.second.tiles);
+    }
+    if (have_dev && !pl->dev.empty()) (void)hipSetDevice(cur);
+    pl->dev.clear();
+  }
+  delete pl;
+}

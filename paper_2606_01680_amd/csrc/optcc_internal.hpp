@@ -1,0 +1,78 @@
+// Internal definitions shared by the host planner and the GPU executor.
+#pragma once
+
+#include <cstdint>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "optcc.h"
+
+namespace optcc {
+
+// One segment as the executor sees it (device table, 32 bytes).
+// Ring sections of the segment occupy [ring_begin, ring_begin + ring_len);
+// section j has qbase + (j < nbig) quanta.  The point-to-point chunk, when
+// present, follows the ring part up to the end of the segment.
+struct SegDesc {
+  int64_t ring_begin;
+  int64_t p2p_begin;
+  int32_t qbase;
+  int32_t nbig;
+  int32_t ordering;  // 1: S1-S2-S3-S4, 2: S3-S1-S4-S2 (Sec. 4.1)
+  int32_t pad;
+};
+static_assert(sizeof(SegDesc) == 32, "SegDesc layout");
+
+// One unit of work for a workgroup: `len` elements from `begin`, all in one
+// segment's ring part (meta & 1 == 0) or its P2P chunk (meta & 1 == 1);
+// meta >> 1 is the segment index.
+struct TileDesc {
+  int64_t begin;
+  int32_t len;
+  int32_t meta;
+};
+static_assert(sizeof(TileDesc) == 16, "TileDesc layout");
+
+constexpr int kQuantum = OPTCC_QUANTUM;
+constexpr int kTileQuanta = 32;  // 2048 elements per tile
+constexpr int kTileElems = kQuantum * kTileQuanta;
+
+struct DeviceTables {
+  SegDesc *segs = nullptr;
+  TileDesc *tiles = nullptr;
+  int64_t ntiles = 0;
+};
+
+struct Segment {
+  int64_t begin = 0, end = 0;          // element range of the segment
+  int64_t ring_begin = 0, ring_end = 0; // ring sections
+  int64_t p2p_begin = 0, p2p_end = 0;   // point-to-point chunk (may be empty)
+  int64_t qbase = 0, nbig = 0;
+  int ordering = 1;
+};
+
+}  // namespace optcc
+
+struct optcc_plan {
+  int p = 0, k = 0, m = 0, kind = 0, pp = 0;
+  int64_t n = 0;
+  std::vector<double> ell;    // slowdown per rank
+  std::vector<int> ring;      // healthy ranks, ascending
+  std::vector<int> strag;     // stragglers, l descending, ties lower rank
+  std::vector<optcc::Segment> seg;
+  std::vector<optcc::SegDesc> segdesc;
+  std::vector<optcc::TileDesc> tiles;
+  int64_t num_steps = 0, num_flows = 0;
+  // device copies of segdesc/tiles, per device ordinal
+  mutable std::mutex mu;
+  mutable std::map<int, optcc::DeviceTables> dev;
+};
+
+namespace optcc {
+void set_error(const std::string &msg);
+int fail(int status, const std::string &msg);
+// Section j's element range inside segment s.
+void section_range(const optcc_plan_t &pl, const Segment &s, int j, int64_t *b, int64_t *e);
+}  // namespace optcc

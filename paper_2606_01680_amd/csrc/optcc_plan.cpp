@@ -1,0 +1,425 @@
+// Host side of the OptCC library: schedule planning, the closed-form model
+// and lower bounds, plan introspection and traffic accounting.  No device
+// calls are made here.
+//
+// Paper: "Don't Let a Few Network Failures Slow the Entire AllReduce".
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "optcc_internal.hpp"
+
+namespace optcc {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string &msg) { g_last_error = msg; }
+
+int fail(int status, const std::string &msg) {
+  set_error(msg);
+  return status;
+}
+
+void section_range(const optcc_plan_t &pl, const Segment &s, int j, int64_t *b, int64_t *e) {
+  int64_t qoff = (int64_t)j * s.qbase + std::min<int64_t>(j, s.nbig);
+  int64_t qlen = s.qbase + (j < s.nbig ? 1 : 0);
+  int64_t lo = s.ring_begin + qoff * kQuantum, hi = lo + qlen * kQuantum;
+  *b = std::min(lo, pl.n);
+  *e = std::min(hi, pl.n);
+}
+
+namespace {
+
+// Sources folded into the chain start before Stage 1 (slot 0) and stragglers
+// that receive the global sum after Stage 4 (slot 5), per section ordering.
+// Ordering 2 (Sec. 4.1): every straggler.  Ordering 1 with m >= 2 (App. D,
+// patterns A'/C'): all but the worst straggler, which finalises in Stages 2/3.
+int n_side(const optcc_plan_t &pl, int ordering) {
+  if (pl.m == 0) return 0;
+  return ordering == 2 ? pl.m : pl.m - 1;
+}
+int side_first(int ordering) { return ordering == 2 ? 0 : 1; }
+
+int ring_at(const optcc_plan_t &pl, int j, int t) {
+  int pp = pl.pp;
+  return pl.ring[(size_t)(((j + t) % pp + pp) % pp)];
+}
+
+// Visit every step in execution order: slot, segment, section (then the
+// point-to-point chunk), hop.  fn(slot, seg, sec, op, dst, srcs, nsrc, off, len).
+template <class Fn>
+void for_each_step(const optcc_plan_t &pl, Fn &&fn) {
+  const int pp = pl.pp;
+  std::vector<int> srcs((size_t)std::max(pl.p, 1));
+  for (int slot = 0; slot < OPTCC_NUM_SLOTS; ++slot) {
+    for (int g = 0; g < pl.k; ++g) {
+      const Segment &s = pl.seg[(size_t)g];
+      const int ord = s.ordering;
+      for (int j = 0; j < pp; ++j) {
+        int64_t b, e;
+        section_range(pl, s, j, &b, &e);
+        if (e <= b) continue;
+        const int holder = ring_at(pl, j, pp - 1);
+        switch (slot) {
+          case 0: {
+            int ns = n_side(pl, ord);
+            if (ns == 0) break;
+            for (int i = 0; i < ns; ++i) srcs[(size_t)i] = pl.strag[(size_t)(side_first(ord) + i)];
+            fn(0, g, j, 1, ring_at(pl, j, 0), srcs.data(), ns, b, e - b);
+            break;
+          }
+          case 1:
+            for (int t = 1; t < pp; ++t) {
+              srcs[0] = ring_at(pl, j, t - 1);
+              fn(1, g, j, 1, ring_at(pl, j, t), srcs.data(), 1, b, e - b);
+            }
+            break;
+          case 2:
+            if (pl.m >= 1 && ord == 1) {
+              srcs[0] = holder;
+              fn(2, g, j, 1, pl.strag[0], srcs.data(), 1, b, e - b);
+            }
+            break;
+          case 3:
+            if (pl.m >= 1 && ord == 1) {
+              srcs[0] = pl.strag[0];
+              fn(3, g, j, 0, holder, srcs.data(), 1, b, e - b);
+            }
+            break;
+          case 4:
+            for (int t = 0; t + 1 < pp; ++t) {
+              srcs[0] = ring_at(pl, j, t - 1);
+              fn(4, g, j, 0, ring_at(pl, j, t), srcs.data(), 1, b, e - b);
+            }
+            break;
+          case 5: {
+            int ns = n_side(pl, ord);
+            for (int i = 0; i < ns; ++i) {
+              srcs[0] = holder;
+              fn(5, g, j, 0, pl.strag[(size_t)(side_first(ord) + i)], srcs.data(), 1, b, e - b);
+            }
+            break;
+          }
+        }
+      }
+      // Bubble filling (Sec. 4.2, App. C): star allreduce through the straggler.
+      if (s.p2p_end > s.p2p_begin) {
+        const int64_t b = s.p2p_begin, len = s.p2p_end - s.p2p_begin;
+        if (slot == 2) {
+          for (int i = 0; i < pp; ++i) srcs[(size_t)i] = pl.ring[(size_t)i];
+          fn(2, g, -1, 1, pl.strag[0], srcs.data(), pp, b, len);
+        } else if (slot == 3) {
+          for (int i = 0; i < pp; ++i) {
+            srcs[0] = pl.strag[0];
+            fn(3, g, -1, 0, pl.ring[(size_t)i], srcs.data(), 1, b, len);
+          }
+        }
+      }
+    }
+  }
+}
+
+// Loads and stores per coordinate that the executor issues for one lane of
+// a section of the given ordering (or of a P2P chunk) over [sb, se) in one
+// launch.  Mirrors the executor's per-lane control flow.
+void lane_traffic(const optcc_plan_t &pl, int ordering, bool p2p, int sb, int se,
+                  int64_t *loads, int64_t *stores) {
+  auto in = [&](int q) { return sb <= q && q < se; };
+  int64_t ld = 0, st = 0;
+  bool have = false;
+  const int64_t pp = pl.pp;
+  if (p2p) {
+    if (in(2)) { ld += 1 + pp; st += 1; have = true; }
+    if (in(3)) { if (!have) ld += 1; st += pp; }
+  } else {
+    const int ns = n_side(pl, ordering);
+    if (in(0) && ns > 0) { ld += 1 + ns; st += 1; have = true; }
+    if (in(1)) { if (!have) ld += 1; ld += pp - 1; st += pp - 1; have = true; }
+    if (pl.m >= 1 && ordering == 1) {
+      if (in(2)) { if (!have) ld += 1; ld += 1; st += 1; have = true; }
+      if (in(3)) { if (!have) ld += 1; st += 1; have = true; }
+    }
+    if (in(4)) { if (!have) ld += 1; st += pp - 1; have = true; }
+    if (in(5) && ns > 0) { if (!have) ld += 1; st += ns; }
+  }
+  *loads = ld;
+  *stores = st;
+}
+
+bool valid_bw(int p, const double *bw, std::string *why) {
+  if (!bw) { *why = "link_bandwidths is NULL"; return false; }
+  for (int i = 0; i < p; ++i)
+    if (!(bw[i] > 0.0) || !std::isfinite(bw[i])) {
+      *why = "link_bandwidths[" + std::to_string(i) + "] must be finite and > 0";
+      return false;
+    }
+  return true;
+}
+
+// Slowdowns l_i = max(b)/b_i and the stragglers sorted by l descending.
+void slowdowns(int p, const double *bw, std::vector<double> *ell, std::vector<int> *strag,
+               std::vector<int> *ring) {
+  double bmax = 0.0;
+  for (int i = 0; i < p; ++i) bmax = std::max(bmax, bw[i]);
+  ell->assign((size_t)p, 1.0);
+  strag->clear();
+  ring->clear();
+  for (int i = 0; i < p; ++i) {
+    (*ell)[(size_t)i] = bmax / bw[i];
+    if (bw[i] < bmax) strag->push_back(i);
+    else ring->push_back(i);
+  }
+  std::stable_sort(strag->begin(), strag->end(),
+                   [&](int a, int b) { return (*ell)[(size_t)a] > (*ell)[(size_t)b]; });
+}
+
+}  // namespace
+}  // namespace optcc
+
+using namespace optcc;
+
+extern "C" const char *optcc_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_t **out) {
+  set_error("");
+  if (!out) return fail(OPTCC_EINVAL, "out is NULL");
+  if (p < 3) return fail(OPTCC_EUNSUPPORTED, "p must be >= 3 (the method needs a straggler and two healthy ranks)");
+  if (p > OPTCC_MAX_RANKS) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_RANKS");
+  if (N < 0 || N > ((int64_t)1 << 46)) return fail(OPTCC_EINVAL, "N must be in [0, 2^46]");
+  if (k < 4 || k % 4 != 0 || k > (1 << 24))
+    return fail(OPTCC_EINVAL, "n_chunks must be a positive multiple of 4 (at most 2^24)");
+  std::string why;
+  if (!valid_bw(p, bw, &why)) return fail(OPTCC_EINVAL, why);
+
+  optcc_plan_t *pl = new (std::nothrow) optcc_plan_t();
+  if (!pl) return fail(OPTCC_ENOMEM, "out of host memory");
+  try {
+    pl->p = p;
+    pl->k = k;
+    pl->n = N;
+    slowdowns(p, bw, &pl->ell, &pl->strag, &pl->ring);
+    pl->m = (int)pl->strag.size();
+    pl->pp = (int)pl->ring.size();
+    if (pl->pp < 2) {
+      delete pl;
+      return fail(OPTCC_EUNSUPPORTED, "fewer than 2 healthy ranks: no ring to reduce-scatter on");
+    }
+    if (pl->m == 0) pl->kind = OPTCC_KIND_RING;
+    else if (pl->m == 1) pl->kind = pl->ell[(size_t)pl->strag[0]] >= 2.0 ? OPTCC_KIND_SINGLE_GE2 : OPTCC_KIND_SINGLE_LT2;
+    else pl->kind = OPTCC_KIND_MULTI;
+
+    const int64_t nq = (N + kQuantum - 1) / kQuantum;
+    pl->seg.resize((size_t)k);
+    pl->segdesc.resize((size_t)k);
+    int64_t steps = 0, flows = 0;
+    for (int g = 0; g < k; ++g) {
+      const int64_t q0 = (int64_t)((__int128)g * nq / k);
+      const int64_t q1 = (int64_t)((__int128)(g + 1) * nq / k);
+      const int64_t lq = q1 - q0;
+      int64_t dq = 0;
+      if (pl->kind == OPTCC_KIND_SINGLE_LT2) {
+        // App. C: D / L = (2-l) / ((p-2) l + 2), rounded to whole quanta.
+        const double l = pl->ell[(size_t)pl->strag[0]];
+        const double x = ((double)lq * (2.0 - l)) / ((double)(p - 2) * l + 2.0);
+        dq = (int64_t)std::floor(x + 0.5);
+        dq = std::max<int64_t>(0, std::min(dq, lq));
+      }
+      const int64_t rq = lq - dq;
+      Segment &s = pl->seg[(size_t)g];
+      s.begin = std::min(q0 * kQuantum, N);
+      s.end = std::min(q1 * kQuantum, N);
+      s.ring_begin = q0 * kQuantum;
+      s.ring_end = std::min((q1 - dq) * kQuantum, N);
+      s.p2p_begin = std::min((q1 - dq) * kQuantum, N);
+      s.p2p_end = s.end;
+      s.qbase = rq / pl->pp;
+      s.nbig = rq % pl->pp;
+      // Patterns (Sec. 4.2; App. D): A,B,C,D or B,D,A',C' by g mod 4.
+      const int pat = g % 4;
+      s.ordering = pl->m <= 1 ? ((pat == 0 || pat == 2) ? 1 : 2) : (pat <= 1 ? 2 : 1);
+      SegDesc &d = pl->segdesc[(size_t)g];
+      d.ring_begin = s.ring_begin;
+      d.p2p_begin = s.p2p_begin;
+      d.qbase = (int32_t)s.qbase;
+      d.nbig = (int32_t)s.nbig;
+      d.ordering = s.ordering;
+      d.pad = 0;
+      // step and flow counts per non-empty section / chunk
+      const int ns = n_side(*pl, s.ordering);
+      const int fin = (pl->m >= 1 && s.ordering == 1) ? 2 : 0;  // Stage 2 + Stage 3 steps
+      // non-empty sections: all with a quantum, unless the segment is cut at N
+      int64_t nonempty = s.qbase > 0 ? pl->pp : s.nbig;
+      if (s.ring_begin + rq * kQuantum > N) {
+        nonempty = 0;
+        for (int j = 0; j < pl->pp; ++j) {
+          int64_t b, e;
+          section_range(*pl, s, j, &b, &e);
+          nonempty += e > b;
+        }
+      }
+      steps += nonempty * ((ns > 0 ? 1 : 0) + 2 * (pl->pp - 1) + fin + ns);
+      flows += nonempty * (ns + 2 * (pl->pp - 1) + fin + ns);
+      if (s.p2p_end > s.p2p_begin) {
+        steps += 1 + pl->pp;
+        flows += 2 * pl->pp;
+      }
+    }
+    pl->num_steps = steps;
+    pl->num_flows = flows;
+  } catch (const std::bad_alloc &) {
+    delete pl;
+    return fail(OPTCC_ENOMEM, "out of host memory");
+  }
+  *out = pl;
+  return OPTCC_OK;
+}
+
+extern "C" int optcc_plan_info(const optcc_plan_t *pl, optcc_plan_info_t *info, int32_t *ring,
+                               int32_t *strag, double *ell) {
+  if (!pl || !info) return fail(OPTCC_EINVAL, "plan and info must be non-NULL");
+  info->p = pl->p;
+  info->k = pl->k;
+  info->m = pl->m;
+  info->kind = pl->kind;
+  info->healthy = pl->pp;
+  info->quantum = kQuantum;
+  info->n = pl->n;
+  info->num_steps = pl->num_steps;
+  info->num_flows = pl->num_flows;
+  if (ring) for (int i = 0; i < pl->pp; ++i) ring[i] = pl->ring[(size_t)i];
+  if (strag) for (int i = 0; i < pl->m; ++i) strag[i] = pl->strag[(size_t)i];
+  if (ell) for (int i = 0; i < pl->p; ++i) ell[i] = pl->ell[(size_t)i];
+  return OPTCC_OK;
+}
+
+extern "C" int optcc_plan_segments(const optcc_plan_t *pl, int64_t *off, int64_t *len,
+                                   int64_t *p2p) {
+  if (!pl || !off || !len || !p2p) return fail(OPTCC_EINVAL, "NULL argument");
+  for (int g = 0; g < pl->k; ++g) {
+    const Segment &s = pl->seg[(size_t)g];
+    off[g] = s.begin;
+    len[g] = s.end - s.begin;
+    p2p[g] = s.p2p_end - s.p2p_begin;
+  }
+  return OPTCC_OK;
+}
+
+extern "C" int64_t optcc_plan_num_flows(const optcc_plan_t *pl) {
+  if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
+  return pl->num_flows;
+}
+
+extern "C" int64_t optcc_plan_get_flows(const optcc_plan_t *pl, optcc_flow_t *out, int64_t cap) {
+  if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
+  if (cap > 0 && !out) return fail(OPTCC_EINVAL, "out is NULL");
+  int64_t nf = 0, step = 0;
+  for_each_step(*pl, [&](int slot, int g, int sec, int op, int dst, const int *srcs, int ns,
+                         int64_t off, int64_t len) {
+    for (int i = 0; i < ns; ++i, ++nf) {
+      if (nf >= cap) continue;
+      optcc_flow_t &f = out[nf];
+      f.slot = slot;
+      f.segment = g;
+      f.section = sec;
+      f.op = op;
+      f.src = srcs[i];
+      f.dst = dst;
+      f.step = step;
+      f.offset = off;
+      f.length = len;
+    }
+    ++step;
+  });
+  return nf;
+}
+
+extern "C" void optcc_plan_free(optcc_plan_t *pl);  // defined with the executor
+
+extern "C" double optcc_model_time(const optcc_plan_t *pl, const double *bw) {
+  if (!pl) { set_error("plan is NULL"); return NAN; }
+  std::vector<double> ell = pl->ell;
+  if (bw) {
+    std::string why;
+    if (!valid_bw(pl->p, bw, &why)) { set_error(why); return NAN; }
+    std::vector<int> strag, ring;
+    slowdowns(pl->p, bw, &ell, &strag, &ring);
+    bool same = strag == pl->strag;
+    for (int i = 0; same && i < pl->p; ++i)
+      same = std::fabs(ell[(size_t)i] - pl->ell[(size_t)i]) <= 1e-12 * pl->ell[(size_t)i];
+    if (!same) {
+      set_error("bandwidths give other stragglers or slowdowns than the plan was built for");
+      return NAN;
+    }
+  }
+  const double p = pl->p, n = (double)pl->n, k = pl->k, m = pl->m;
+  switch (pl->kind) {
+    case OPTCC_KIND_RING:
+      return 2.0 * (p - 1.0) * n / p;  // T0 (Sec. 3)
+    case OPTCC_KIND_SINGLE_GE2: {
+      const double l = ell[(size_t)pl->strag[0]];
+      return l * n * (k + 1.0) / k;  // Sec. 4.3, l >= 2
+    }
+    case OPTCC_KIND_SINGLE_LT2: {
+      const double l = ell[(size_t)pl->strag[0]];
+      return 2.0 * (p - 1.0) * l * n / ((p - 2.0) * l + 2.0) * (k + l - 1.0) / k;  // App. C
+    }
+    default: {
+      const double l1 = ell[(size_t)pl->strag[0]];
+      const double s = n / (k * (p - m));
+      const double body = std::max(2.0 * (p - 1.0) * s, (l1 * (p - m) + 2.0 * (m - 1.0)) * s);
+      return (k + 4.0) * body;  // App. D
+    }
+  }
+}
+
+extern "C" double optcc_lower_bound(int p, const double *bw, int64_t N) {
+  if (p < 3 || p > OPTCC_MAX_RANKS) { set_error("p must be in [3, OPTCC_MAX_RANKS]"); return NAN; }
+  if (N < 0) { set_error("N must be >= 0"); return NAN; }
+  std::string why;
+  if (!valid_bw(p, bw, &why)) { set_error(why); return NAN; }
+  std::vector<double> ell;
+  std::vector<int> strag, ring;
+  slowdowns(p, bw, &ell, &strag, &ring);
+  const double n = (double)N, P = p;
+  const size_t m = strag.size();
+  if (m == 0) return 2.0 * (P - 1.0) * n / P;
+  const double l1 = ell[(size_t)strag[0]];
+  if (m == 1) return std::max(2.0 * l1 * (P - 1.0) / (l1 * (P - 2.0) + 2.0), l1) * n;
+  double inv = 0.0;
+  for (int r : strag) inv += 1.0 / ell[(size_t)r];
+  return std::max(2.0 * (P - 1.0) / (P - (double)m + inv), l1) * n;
+}
+
+extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, int sb, int se,
+                                  int launches, int64_t *rd, int64_t *wr) {
+  if (!pl || !rd || !wr) return fail(OPTCC_EINVAL, "NULL argument");
+  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
+    return fail(OPTCC_EINVAL, "unknown dtype");
+  if (sb < 0 || se > OPTCC_NUM_SLOTS || sb > se) return fail(OPTCC_EINVAL, "bad slot range");
+  const int64_t es = dtype == OPTCC_BF16 ? 2 : 4;
+  int64_t r = 0, w = 0;
+  auto add = [&](int ord, bool p2p, int64_t len) {
+    if (launches == 1) {
+      int64_t l, s;
+      lane_traffic(*pl, ord, p2p, sb, se, &l, &s);
+      r += l * len;
+      w += s * len;
+    } else {
+      for (int q = sb; q < se; ++q) {
+        int64_t l, s;
+        lane_traffic(*pl, ord, p2p, q, q + 1, &l, &s);
+        r += l * len;
+        w += s * len;
+      }
+    }
+  };
+  for (const Segment &s : pl->seg) {
+    add(s.ordering, false, s.ring_end > s.ring_begin ? s.ring_end - std::min(s.ring_begin, s.ring_end) : 0);
+    add(s.ordering, true, s.p2p_end - s.p2p_begin);
+  }
+  *rd = r * es;
+  *wr = w * es;
+  return OPTCC_OK;
+}

@@ -1,0 +1,190 @@
+"""GPU parity: the HIP executor against the oracle, through the C ABI.
+
+Small cases compare every element of every rank bit for bit with the oracle's
+serial execution (fp32, bf16 and int32 alike: the schedule fixes the
+reduction order).  Slot prefixes check that every step is materialised in its
+destination buffer, stage by stage.  Full-size workloads are checked at
+sampled coordinates against the oracle, and everywhere through properties that
+hold at any size (all ranks identical, exact int32 sums, the fp error bound).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import bits_equal, rand_inputs, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def o():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_01680_amd import optcc
+    return optcc
+
+
+def _bw(p, slow):
+    b = [1.0] * p
+    for r, v in slow.items():
+        b[r] = v
+    return b
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+PROFILES = [
+    (3, {}), (3, {2: 0.5}), (4, {3: 0.5}), (5, {0: 0.5}), (5, {2: 0.75}), (8, {7: 0.875}),
+    (8, {3: 0.25}), (6, {0: 0.5, 5: 0.75}), (9, {0: 0.875, 3: 0.75, 8: 0.5}), (16, {15: 0.5}),
+    (12, {}), (20, {1: 0.5, 2: 0.5, 19: 0.9}), (40, {5: 0.6}),
+]
+# sizes span several 2048-element tiles, ragged tails, empty sections
+SIZES = [(1, 4), (37, 4), (64, 4), (1000, 8), (2048 * 3 + 64 * 5 + 3, 8), (40000, 12)]
+
+
+def _run_both(o, p, slow, n, k, dtype, seed, kind="normal", slot_end=6, launches=1):
+    bw = _bw(p, slow)
+    x = rand_inputs(dtype, p, n, seed, kind)
+    ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy(), 0, slot_end)
+    pl = o.optcc_plan(p, bw, n, k)
+    d = to_device(x, dtype)
+    o.optcc_allreduce_emulate_slots(d, p, n, dtype, pl, 0, slot_end, launches)
+    torch.cuda.synchronize()
+    return x, ref, to_host(d, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("p,slow", PROFILES)
+@pytest.mark.parametrize("n,k", SIZES)
+def test_small_bit_exact(o, dtype, p, slow, n, k):
+    _say(f"case dtype={dtype} p={p} slow={slow} n={n} k={k}")
+    x, ref, got = _run_both(o, p, slow, n, k, dtype, seed=p * 1000 + n)
+    assert bits_equal(got, ref)
+    if n:
+        assert (got == got[0][None, :]).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("p,slow", [(5, {0: 0.5}), (8, {7: 0.875}), (9, {0: 0.875, 3: 0.75, 8: 0.5}),
+                                    (7, {}), (6, {1: 0.25, 2: 0.5})])
+@pytest.mark.parametrize("launches", [1, 0])
+def test_stage_snapshots(o, dtype, p, slow, launches):
+    """After the first s slots (s = 1..6), in one fused launch or one launch
+    per slot, every buffer equals the oracle's state after the same slots:
+    every step's destination write is materialised."""
+    n, k = 2048 * 2 + 64 * 7 + 5, 8
+    for s in range(1, 7):
+        _say(f"case snapshot dtype={dtype} p={p} slots=[0,{s}) launches={launches}")
+        x, ref, got = _run_both(o, p, slow, n, k, dtype, seed=17 + s, slot_end=s, launches=launches)
+        assert bits_equal(got, ref), f"slots [0,{s})"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["denormal", "wide"])
+def test_special_values(o, dtype, kind):
+    """Subnormal inputs (no flush to zero on either side) and values spread
+    over 120 binades (heavy cancellation) stay bit-exact."""
+    for p, slow in [(5, {0: 0.5}), (8, {7: 0.875}), (9, {0: 0.875, 3: 0.75, 8: 0.5})]:
+        _say(f"case special {kind} dtype={dtype} p={p}")
+        x, ref, got = _run_both(o, p, slow, 5000, 8, dtype, seed=3, kind=kind)
+        assert bits_equal(got, ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+def test_unaligned_buffers(o, dtype):
+    """Rank buffers that are only element-aligned take the one-element path."""
+    p, n, k = 8, 3000, 8
+    bw = _bw(p, {7: 0.875})
+    x = rand_inputs(dtype, p, n, 5)
+    ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+    pl = o.optcc_plan(p, bw, n, k)
+    stride = n + 1  # rank r starts at 1 + r*(n+1) elements: not 16-byte aligned
+    flat = torch.zeros(p * stride + 8, dtype=to_device(x[:1, :1], dtype).dtype, device="cuda:0")
+    for r in range(p):
+        flat[1 + r * stride: 1 + r * stride + n].copy_(to_device(x[r:r + 1], dtype)[0])
+    views = [flat[1 + r * stride: 1 + r * stride + n] for r in range(p)]
+    _say(f"case unaligned dtype={dtype}")
+    o.optcc_allreduce_emulate(views, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    got = np.stack([to_host(v, dtype) for v in views])
+    assert bits_equal(got, ref)
+
+
+def test_deterministic_and_stream(o):
+    """Same inputs, same bits, on the default stream and a side stream."""
+    p, n, k = 9, 50000, 8
+    bw = _bw(p, {0: 0.875, 3: 0.75, 8: 0.5})
+    x = rand_inputs("f32", p, n, 9)
+    pl = o.optcc_plan(p, bw, n, k)
+    a = to_device(x, "f32")
+    b = to_device(x, "f32")
+    o.optcc_allreduce_emulate(a, p, n, "f32", pl)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        o.optcc_allreduce_emulate(b, p, n, "f32", pl, stream=s)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+# ----------------------------------------------------------- full workloads
+def _sample_coords(plan, n, rng, count=4096):
+    """Random coordinates plus every segment's first and last element, both
+    sides of each P2P chunk boundary and the vector's ends."""
+    off, ln, p2p = plan.segments()
+    picks = set(rng.integers(0, n, size=count).tolist())
+    for g in range(len(off)):
+        b, e = int(off[g]), int(off[g] + ln[g])
+        for c in (b, e - 1, e - int(p2p[g]), e - int(p2p[g]) - 1):
+            if 0 <= c < n:
+                picks.add(c)
+    picks.update([0, n - 1])
+    return np.array(sorted(picks), dtype=np.int64)
+
+
+WORKLOADS = ["p4_f32", "p8_f32", "p8_i32", "p16_bf16", "p64_f32", "p128_f32"]
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_workload_full_size(o, name):
+    from paper_2606_01680_amd.workloads import WORKLOADS as W, make_inputs
+    w = W[name]
+    _say(f"case workload {name} p={w.p} N={w.n} dtype={w.dtype} k={w.k}")
+    x = make_inputs(w, device="cuda:0")
+    x0 = x.clone()
+    pl = o.optcc_plan(w.p, w.bandwidths, w.n, w.k)
+    o.optcc_allreduce_emulate(x, w.p, w.n, w.dtype, pl)
+    torch.cuda.synchronize()
+    iv = x.view(torch.int16) if w.dtype == "bf16" else x.view(torch.int32)
+    for r in range(1, w.p):  # every rank holds the same bits
+        assert torch.equal(iv[r], iv[0]), r
+    rng = np.random.default_rng(1234)
+    coords = _sample_coords(pl, w.n, rng)
+    idx = torch.from_numpy(coords).to("cuda:0")
+    cols = to_host(x0[:, idx], w.dtype).copy()
+    sched = oracle.Schedule(w.p, w.bandwidths, w.n, w.k)
+    oracle.run_sampled(sched, w.dtype, cols, coords)
+    got = to_host(x[:, idx], w.dtype)
+    assert bits_equal(got, cols)
+    # properties over every coordinate, chunked
+    step = max(1 << 16, (1 << 28) // w.p)
+    for c0 in range(0, w.n, step):
+        c1 = min(w.n, c0 + step)
+        if w.dtype == "i32":
+            want = x0[:, c0:c1].to(torch.int64).sum(0)
+            want = ((want + 2**31) % 2**32 - 2**31).to(torch.int32)
+            assert torch.equal(x[0, c0:c1], want)
+        else:
+            xs = x0[:, c0:c1].to(torch.float64)
+            err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
+            u = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8
+            assert bool((err <= w.p * u * xs.abs().sum(0)).all())
+    if w.n <= 1 << 16:  # small enough for the oracle's full run
+        full = oracle.run(sched, w.dtype, to_host(x0, w.dtype).copy())
+        assert bits_equal(to_host(x, w.dtype), full)
