@@ -73,6 +73,25 @@ def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
                       f"serial C oracle, {t:.2f} s"}
 
 
+def copy_bench(torch, args):
+    """A plain copy of a known size: reads and writes copy_bytes each."""
+    src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    print(json.dumps({"copy_bytes": args.copy_bytes, "ms": round(ms, 5),
+                      "GBps_read_plus_write": round(2 * args.copy_bytes / (ms * 1e-3) / 1e9, 2)}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -83,6 +102,10 @@ def main():
                     help="1: fused (default); 0: one launch per stage slot")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--copy-only", action="store_true",
+                    help="time torch's plain device-to-device copy instead (the reference "
+                         "kernel for scaling rocprofv3 byte counters)")
+    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: the OptCC emulation runs the p logical ranks on ONE GPU; "
@@ -97,6 +120,9 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.copy_only:
+        copy_bench(torch, args)
+        return
     w = WORKLOADS[args.workload]
     x = make_inputs(w, device="cuda:0")
     x0 = x.clone()
@@ -177,6 +203,9 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
+            "traffic_GBps": None if traffic is None else round(traffic / (ms_launch * 1e-3) / 1e9, 2),
+            "traffic_frac": None if traffic is None else round(
+                traffic / (ms_launch * 1e-3) / 1e9 / PEAK_GBPS, 4),
             "algorithmic_bytes": alg_bytes, "read_bytes": rd, "write_bytes": wr,
             "kernel_ms": round(ms_launch, 5), "kernel": "optcc_exec_kernel",
         },
