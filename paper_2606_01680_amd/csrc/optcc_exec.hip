@@ -30,9 +30,32 @@
 namespace optcc {
 namespace {
 
+#ifndef OPTCC_HOP_BATCH
+#define OPTCC_HOP_BATCH 16
+#endif
+#ifndef OPTCC_NT_LOADS
+#define OPTCC_NT_LOADS 1
+#endif
+#ifndef OPTCC_NT_FINAL
+#define OPTCC_NT_FINAL 1
+#endif
+#ifndef OPTCC_NT_MID
+#define OPTCC_NT_MID 0
+#endif
+#ifndef OPTCC_MIN_WAVES
+#define OPTCC_MIN_WAVES 1
+#endif
+
 constexpr int kThreads = 256;
 constexpr int kMaxRanks = OPTCC_MAX_EMULATE_RANKS;
-constexpr int kHopBatch = 8;  // loads in flight per vector along a chain
+constexpr int kHopBatch = OPTCC_HOP_BATCH;  // loads in flight per vector along a chain
+// Input values are read once: streaming (nontemporal) loads keep them from
+// displacing lines in L2.  Stores of values that no later step overwrites
+// are streamed too; Stage-1 partials that Stage 4 overwrites are ordinary
+// stores, so that L2 can absorb the first write.
+constexpr bool kNtLoads = OPTCC_NT_LOADS;
+constexpr bool kNtFinal = OPTCC_NT_FINAL;
+constexpr bool kNtMid = OPTCC_NT_MID;
 
 struct KArgs {
   const TileDesc *tiles;
@@ -78,13 +101,50 @@ struct alignas(sizeof(typename D::S) * W) Vec {
   typename D::S v[W];
 };
 
-template <class D, int W>
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Loads and stores of W elements; NT selects the streaming hint.
+template <class D, int W, bool NT = false>
 __device__ __forceinline__ Vec<D, W> vload(const void *base, int64_t e) {
-  return *reinterpret_cast<const Vec<D, W> *>(static_cast<const typename D::S *>(base) + e);
+  const typename D::S *p = static_cast<const typename D::S *>(base) + e;
+  if constexpr (sizeof(Vec<D, W>) == 16) {
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+    const u32x4 r = NT ? __builtin_nontemporal_load(q) : *q;
+    return __builtin_bit_cast(Vec<D, W>, r);
+  } else {
+    static_assert(W == 1, "vectors are 16 bytes or one element");
+    Vec<D, W> r;
+    r.v[0] = NT ? __builtin_nontemporal_load(p) : *p;
+    return r;
+  }
+}
+template <class D, int W, bool NT = false>
+__device__ __forceinline__ void vstore(void *base, int64_t e, const Vec<D, W> &x) {
+  typename D::S *p = static_cast<typename D::S *>(base) + e;
+  if constexpr (sizeof(Vec<D, W>) == 16) {
+    u32x4 *q = reinterpret_cast<u32x4 *>(p);
+    const u32x4 v = __builtin_bit_cast(u32x4, x);
+    if (NT) __builtin_nontemporal_store(v, q);
+    else *q = v;
+  } else {
+    static_assert(W == 1, "vectors are 16 bytes or one element");
+    if (NT) __builtin_nontemporal_store(x.v[0], p);
+    else *p = x.v[0];
+  }
+}
+// input loads and final stores with the configured hints
+template <class D, int W>
+__device__ __forceinline__ Vec<D, W> ld_in(const void *base, int64_t e) {
+  return vload<D, W, kNtLoads>(base, e);
 }
 template <class D, int W>
-__device__ __forceinline__ void vstore(void *base, int64_t e, const Vec<D, W> &x) {
-  *reinterpret_cast<Vec<D, W> *>(static_cast<typename D::S *>(base) + e) = x;
+__device__ __forceinline__ void st_fin(void *base, int64_t e, const Vec<D, W> &x) {
+  vstore<D, W, kNtFinal>(base, e, x);
+}
+// stores of values a later step of the same section overwrites
+template <class D, int W>
+__device__ __forceinline__ void st_mid(void *base, int64_t e, const Vec<D, W> &x) {
+  vstore<D, W, kNtMid>(base, e, x);
 }
 // One reduce step with a single source: narrow(widen(a) + widen(b)).
 template <class D, int W>
@@ -142,58 +202,56 @@ __device__ void ring_lane(const KArgs &a, void *const *rp, const SegDesc &sd, in
   // Stage 2's straggler operand does not depend on the chain: load it early.
   V xs;
   const bool do2 = fin && in_range(a, 2);
-  if (do2) xs = vload<D, W>(a.ptr[pp], e);
+  if (do2) xs = ld_in<D, W>(a.ptr[pp], e);
 
   if (in_range(a, 0) && nside > 0) {  // slot 0
-    AccV<D, W> acc = widen(vload<D, W>(rp[j], e));
-    for (int i = 0; i < nside; ++i) accum(acc, vload<D, W>(a.ptr[pp + sfirst + i], e));
+    AccV<D, W> acc = widen(ld_in<D, W>(rp[j], e));
+    for (int i = 0; i < nside; ++i) accum(acc, ld_in<D, W>(a.ptr[pp + sfirst + i], e));
     v = narrow(acc);
-    vstore<D, W>(rp[j], e, v);
+    st_mid<D, W>(rp[j], e, v);
     have = true;
   }
-  if (in_range(a, 1)) {  // slot 1: Stage 1 chain, loads kHopBatch hops ahead
-    if (!have) v = vload<D, W>(rp[j], e);
+  if (in_range(a, 1)) {  // slot 1: Stage 1 chain
+    if (!have) v = ld_in<D, W>(rp[j], e);
+    // The hop loads are independent of the partial: keep kHopBatch of them
+    // in flight in a rolling window, refilling a slot as soon as it is used.
     const int nh = pp - 1;
-    V cur[kHopBatch], nxt[kHopBatch];
+    V buf[kHopBatch];
 #pragma unroll
     for (int u = 0; u < kHopBatch; ++u)
-      if (u < nh) cur[u] = vload<D, W>(rp[pos(1 + u)], e);
+      if (u < nh) buf[u] = ld_in<D, W>(rp[pos(1 + u)], e);
     for (int t = 0; t < nh; t += kHopBatch) {
 #pragma unroll
       for (int u = 0; u < kHopBatch; ++u)
-        if (t + kHopBatch + u < nh) nxt[u] = vload<D, W>(rp[pos(1 + t + kHopBatch + u)], e);
-#pragma unroll
-      for (int u = 0; u < kHopBatch; ++u)
         if (t + u < nh) {
-          v = add2<D, W>(cur[u], v);
-          vstore<D, W>(rp[pos(1 + t + u)], e, v);
+          v = add2<D, W>(buf[u], v);
+          st_mid<D, W>(rp[pos(1 + t + u)], e, v);
+          if (t + u + kHopBatch < nh) buf[u] = ld_in<D, W>(rp[pos(1 + t + u + kHopBatch)], e);
         }
-#pragma unroll
-      for (int u = 0; u < kHopBatch; ++u) cur[u] = nxt[u];
     }
     have = true;
   }
   if (fin) {
     if (do2) {  // slot 2: straggler <- straggler + holder's partial
-      if (!have) v = vload<D, W>(holder, e);
+      if (!have) v = ld_in<D, W>(holder, e);
       v = add2<D, W>(xs, v);
-      vstore<D, W>(a.ptr[pp], e, v);
+      st_fin<D, W>(a.ptr[pp], e, v);
       have = true;
     }
     if (in_range(a, 3)) {  // slot 3: holder <- global sum
-      if (!have) v = vload<D, W>(a.ptr[pp], e);
-      vstore<D, W>(holder, e, v);
+      if (!have) v = ld_in<D, W>(a.ptr[pp], e);
+      st_fin<D, W>(holder, e, v);
       have = true;
     }
   }
   if (in_range(a, 4)) {  // slot 4: allgather
-    if (!have) v = vload<D, W>(holder, e);
-    for (int t = 0; t + 1 < pp; ++t) vstore<D, W>(rp[pos(t)], e, v);
+    if (!have) v = ld_in<D, W>(holder, e);
+    for (int t = 0; t + 1 < pp; ++t) st_fin<D, W>(rp[pos(t)], e, v);
     have = true;
   }
   if (in_range(a, 5) && nside > 0) {  // slot 5
-    if (!have) v = vload<D, W>(holder, e);
-    for (int i = 0; i < nside; ++i) vstore<D, W>(a.ptr[pp + sfirst + i], e, v);
+    if (!have) v = ld_in<D, W>(holder, e);
+    for (int i = 0; i < nside; ++i) st_fin<D, W>(a.ptr[pp + sfirst + i], e, v);
   }
 }
 
@@ -207,23 +265,23 @@ __device__ void p2p_lane(const KArgs &a, void *const *rp, int64_t e) {
   V g;
   bool have = false;
   if (in_range(a, 2)) {
-    AccV<D, W> acc = widen(vload<D, W>(a.ptr[pp], e));
+    AccV<D, W> acc = widen(ld_in<D, W>(a.ptr[pp], e));
     for (int t = 0; t < pp; t += kHopBatch) {
       V x[kHopBatch];
 #pragma unroll
       for (int u = 0; u < kHopBatch; ++u)
-        if (t + u < pp) x[u] = vload<D, W>(rp[t + u], e);
+        if (t + u < pp) x[u] = ld_in<D, W>(rp[t + u], e);
 #pragma unroll
       for (int u = 0; u < kHopBatch; ++u)
         if (t + u < pp) accum(acc, x[u]);
     }
     g = narrow(acc);
-    vstore<D, W>(a.ptr[pp], e, g);
+    st_fin<D, W>(a.ptr[pp], e, g);
     have = true;
   }
   if (in_range(a, 3)) {
-    if (!have) g = vload<D, W>(a.ptr[pp], e);
-    for (int i = 0; i < pp; ++i) vstore<D, W>(rp[i], e, g);
+    if (!have) g = ld_in<D, W>(a.ptr[pp], e);
+    for (int i = 0; i < pp; ++i) st_fin<D, W>(rp[i], e, g);
   }
 }
 
@@ -250,7 +308,7 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
 // aligned, else 1 element.  Elements of a tile past a whole vector (only at
 // the end of the rank vectors) go one by one.
 template <class D, int W>
-__global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
+__global__ __launch_bounds__(kThreads, OPTCC_MIN_WAVES) void optcc_exec_kernel(KArgs a) {
   __shared__ void *rp[kMaxRanks];
   for (int i = threadIdx.x; i < a.pp; i += kThreads) rp[i] = a.ptr[i];
   __syncthreads();

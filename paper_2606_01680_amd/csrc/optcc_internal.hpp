@@ -35,8 +35,11 @@ struct TileDesc {
 };
 static_assert(sizeof(TileDesc) == 16, "TileDesc layout");
 
+#ifndef OPTCC_TILE_QUANTA
+#define OPTCC_TILE_QUANTA 32
+#endif
 constexpr int kQuantum = OPTCC_QUANTUM;
-constexpr int kTileQuanta = 32;  // 2048 elements per tile
+constexpr int kTileQuanta = OPTCC_TILE_QUANTA;  // 2048 elements per tile by default
 constexpr int kTileElems = kQuantum * kTileQuanta;
 
 struct DeviceTables {
