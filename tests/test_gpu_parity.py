@@ -1,11 +1,12 @@
 """GPU parity: the HIP executor against the oracle, through the C ABI.
 
-Small cases compare every element of every rank bit for bit with the oracle's
-serial execution (fp32, bf16 and int32 alike: the schedule fixes the
-reduction order).  Slot prefixes check that every step is materialised in its
-destination buffer, stage by stage.  Full-size workloads are checked at
-sampled coordinates against the oracle, and everywhere through properties that
-hold at any size (all ranks identical, exact int32 sums, the fp error bound).
+Every case compares every element of every rank bit for bit with the
+oracle's serial execution (fp32, bf16 and int32 alike: the schedule fixes the
+reduction order), from small ragged cases to the full-size workloads.  Slot
+prefixes check that every step is materialised in its destination buffer,
+stage by stage.  Full-size runs also check properties that hold at any size
+(all ranks identical, exact int32 sums, the fp error bound) and sampled
+coordinates through the oracle's per-coordinate executor.
 """
 import sys
 
@@ -185,6 +186,9 @@ def test_workload_full_size(o, name):
             err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
             u = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8
             assert bool((err <= w.p * u * xs.abs().sum(0)).all())
-    if w.n <= 1 << 16:  # small enough for the oracle's full run
-        full = oracle.run(sched, w.dtype, to_host(x0, w.dtype).copy())
-        assert bits_equal(to_host(x, w.dtype), full)
+    # and every element of every rank against the oracle's full serial run
+    _say(f"case workload {name}: full oracle run")
+    full = oracle.run(sched, w.dtype, to_host(x0, w.dtype).copy())
+    del x0
+    got_all = to_host(x, w.dtype)
+    assert bits_equal(got_all, full)
