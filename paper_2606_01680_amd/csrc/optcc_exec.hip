@@ -30,9 +30,6 @@
 namespace optcc {
 namespace {
 
-#ifndef OPTCC_HOP_BATCH
-#define OPTCC_HOP_BATCH 16
-#endif
 #ifndef OPTCC_NT_LOADS
 #define OPTCC_NT_LOADS 1
 #endif
@@ -42,13 +39,10 @@ namespace {
 #ifndef OPTCC_NT_MID
 #define OPTCC_NT_MID 0
 #endif
-#ifndef OPTCC_MIN_WAVES
-#define OPTCC_MIN_WAVES 1
-#endif
 
 constexpr int kThreads = 256;
 constexpr int kMaxRanks = OPTCC_MAX_EMULATE_RANKS;
-constexpr int kHopBatch = OPTCC_HOP_BATCH;  // loads in flight per vector along a chain
+constexpr int kHopWindow = 16;  // hop loads in flight per vector along a chain
 // Input values are read once: streaming (nontemporal) loads keep them from
 // displacing lines in L2.  Stores of values that no later step overwrites
 // are streamed too; Stage-1 partials that Stage 4 overwrites are ordinary
@@ -56,6 +50,9 @@ constexpr int kHopBatch = OPTCC_HOP_BATCH;  // loads in flight per vector along 
 constexpr bool kNtLoads = OPTCC_NT_LOADS;
 constexpr bool kNtFinal = OPTCC_NT_FINAL;
 constexpr bool kNtMid = OPTCC_NT_MID;
+// fp32/int32 plans with at most this many healthy ranks run two 16-byte
+// vectors per lane in lockstep (measured faster for short chains)
+constexpr int kTwoVectorMaxHealthy = 32;
 
 struct KArgs {
   const TileDesc *tiles;
@@ -181,107 +178,165 @@ __device__ __forceinline__ Vec<D, W> narrow(const AccV<D, W> &a) {
 __device__ __forceinline__ bool in_range(const KArgs &a, int q) { return a.sb <= q && q < a.se; }
 
 // ------------------------------------------------------- one ring section
-// Every step of section j (segment descriptor sd) for the W elements at e.
+// Every step of the ring sections for L vectors of W elements per lane, in
+// lockstep: vector l starts at element e[l] and lies in section j[l].
 // rp[i] is the i-th healthy rank's buffer in ring order (LDS copy).
-template <class D, int W>
-__device__ void ring_lane(const KArgs &a, void *const *rp, const SegDesc &sd, int j, int64_t e) {
+template <class D, int W, int L, int B>
+__device__ void ring_lane(const KArgs &a, void *const *rp, const SegDesc &sd, const int (&j)[L],
+                          const int64_t (&e)[L]) {
   using V = Vec<D, W>;
   const int pp = a.pp, m = a.m;
   const int ord = sd.ordering;
   const int nside = m == 0 ? 0 : (ord == 2 ? m : m - 1);
   const int sfirst = ord == 2 ? 0 : 1;
   const bool fin = m >= 1 && ord == 1;  // a straggler finalises in Stages 2/3
-  auto pos = [&](int t) {               // ring position of R[j + t], 0 <= t < 2 pp
-    int i = j + t;
-    return i >= pp ? i - pp : i;
+  auto rank = [&](int l, int t) {       // buffer of R[j[l] + t], 0 <= t < 2 pp
+    int i = j[l] + t;
+    return rp[i >= pp ? i - pp : i];
   };
-  void *const holder = rp[pos(pp - 1)];
-  V v;
+  void *holder[L];
+#pragma unroll
+  for (int l = 0; l < L; ++l) holder[l] = rank(l, pp - 1);
+  V v[L];
   bool have = false;
 
   // Stage 2's straggler operand does not depend on the chain: load it early.
-  V xs;
+  V xs[L];
   const bool do2 = fin && in_range(a, 2);
-  if (do2) xs = ld_in<D, W>(a.ptr[pp], e);
+  if (do2) {
+#pragma unroll
+    for (int l = 0; l < L; ++l) xs[l] = ld_in<D, W>(a.ptr[pp], e[l]);
+  }
 
   if (in_range(a, 0) && nside > 0) {  // slot 0
-    AccV<D, W> acc = widen(ld_in<D, W>(rp[j], e));
-    for (int i = 0; i < nside; ++i) accum(acc, ld_in<D, W>(a.ptr[pp + sfirst + i], e));
-    v = narrow(acc);
-    st_mid<D, W>(rp[j], e, v);
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      AccV<D, W> acc = widen(ld_in<D, W>(rp[j[l]], e[l]));
+      for (int i = 0; i < nside; ++i) accum(acc, ld_in<D, W>(a.ptr[pp + sfirst + i], e[l]));
+      v[l] = narrow(acc);
+      st_mid<D, W>(rp[j[l]], e[l], v[l]);
+    }
     have = true;
   }
   if (in_range(a, 1)) {  // slot 1: Stage 1 chain
-    if (!have) v = ld_in<D, W>(rp[j], e);
-    // The hop loads are independent of the partial: keep kHopBatch of them
+    if (!have) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) v[l] = ld_in<D, W>(rp[j[l]], e[l]);
+    }
+    // The hop loads are independent of the partial: keep B of them
     // in flight in a rolling window, refilling a slot as soon as it is used.
     const int nh = pp - 1;
-    V buf[kHopBatch];
+    V buf[B][L];
 #pragma unroll
-    for (int u = 0; u < kHopBatch; ++u)
-      if (u < nh) buf[u] = ld_in<D, W>(rp[pos(1 + u)], e);
-    for (int t = 0; t < nh; t += kHopBatch) {
+    for (int u = 0; u < B; ++u)
+      if (u < nh) {
 #pragma unroll
-      for (int u = 0; u < kHopBatch; ++u)
+        for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W>(rank(l, 1 + u), e[l]);
+      }
+    for (int t = 0; t < nh; t += B) {
+#pragma unroll
+      for (int u = 0; u < B; ++u)
         if (t + u < nh) {
-          v = add2<D, W>(buf[u], v);
-          st_mid<D, W>(rp[pos(1 + t + u)], e, v);
-          if (t + u + kHopBatch < nh) buf[u] = ld_in<D, W>(rp[pos(1 + t + u + kHopBatch)], e);
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            v[l] = add2<D, W>(buf[u][l], v[l]);
+            st_mid<D, W>(rank(l, 1 + t + u), e[l], v[l]);
+          }
+          if (t + u + B < nh) {
+#pragma unroll
+            for (int l = 0; l < L; ++l)
+              buf[u][l] = ld_in<D, W>(rank(l, 1 + t + u + B), e[l]);
+          }
         }
     }
     have = true;
   }
   if (fin) {
     if (do2) {  // slot 2: straggler <- straggler + holder's partial
-      if (!have) v = ld_in<D, W>(holder, e);
-      v = add2<D, W>(xs, v);
-      st_fin<D, W>(a.ptr[pp], e, v);
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        if (!have) v[l] = ld_in<D, W>(holder[l], e[l]);
+        v[l] = add2<D, W>(xs[l], v[l]);
+        st_fin<D, W>(a.ptr[pp], e[l], v[l]);
+      }
       have = true;
     }
     if (in_range(a, 3)) {  // slot 3: holder <- global sum
-      if (!have) v = ld_in<D, W>(a.ptr[pp], e);
-      st_fin<D, W>(holder, e, v);
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        if (!have) v[l] = ld_in<D, W>(a.ptr[pp], e[l]);
+        st_fin<D, W>(holder[l], e[l], v[l]);
+      }
       have = true;
     }
   }
   if (in_range(a, 4)) {  // slot 4: allgather
-    if (!have) v = ld_in<D, W>(holder, e);
-    for (int t = 0; t + 1 < pp; ++t) st_fin<D, W>(rp[pos(t)], e, v);
+    if (!have) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) v[l] = ld_in<D, W>(holder[l], e[l]);
+    }
+    for (int t = 0; t + 1 < pp; ++t) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(rank(l, t), e[l], v[l]);
+    }
     have = true;
   }
   if (in_range(a, 5) && nside > 0) {  // slot 5
-    if (!have) v = ld_in<D, W>(holder, e);
-    for (int i = 0; i < nside; ++i) st_fin<D, W>(a.ptr[pp + sfirst + i], e, v);
+    if (!have) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) v[l] = ld_in<D, W>(holder[l], e[l]);
+    }
+    for (int i = 0; i < nside; ++i) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(a.ptr[pp + sfirst + i], e[l], v[l]);
+    }
   }
 }
 
 // ------------------------------------------------- one point-to-point chunk
 // Bubble filling (Sec. 4.2, App. C): the straggler sums its own value and
 // R[0..P'-1] in that order, rounding once, and broadcasts the result.
-template <class D, int W>
-__device__ void p2p_lane(const KArgs &a, void *const *rp, int64_t e) {
+template <class D, int W, int L, int B>
+__device__ void p2p_lane(const KArgs &a, void *const *rp, const int64_t (&e)[L]) {
   using V = Vec<D, W>;
   const int pp = a.pp;
-  V g;
+  V g[L];
   bool have = false;
   if (in_range(a, 2)) {
-    AccV<D, W> acc = widen(ld_in<D, W>(a.ptr[pp], e));
-    for (int t = 0; t < pp; t += kHopBatch) {
-      V x[kHopBatch];
+    AccV<D, W> acc[L];
 #pragma unroll
-      for (int u = 0; u < kHopBatch; ++u)
-        if (t + u < pp) x[u] = ld_in<D, W>(rp[t + u], e);
+    for (int l = 0; l < L; ++l) acc[l] = widen(ld_in<D, W>(a.ptr[pp], e[l]));
+    for (int t = 0; t < pp; t += B) {
+      V x[B][L];
 #pragma unroll
-      for (int u = 0; u < kHopBatch; ++u)
-        if (t + u < pp) accum(acc, x[u]);
+      for (int u = 0; u < B; ++u)
+        if (t + u < pp) {
+#pragma unroll
+          for (int l = 0; l < L; ++l) x[u][l] = ld_in<D, W>(rp[t + u], e[l]);
+        }
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (t + u < pp) {
+#pragma unroll
+          for (int l = 0; l < L; ++l) accum(acc[l], x[u][l]);
+        }
     }
-    g = narrow(acc);
-    st_fin<D, W>(a.ptr[pp], e, g);
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      g[l] = narrow(acc[l]);
+      st_fin<D, W>(a.ptr[pp], e[l], g[l]);
+    }
     have = true;
   }
   if (in_range(a, 3)) {
-    if (!have) g = ld_in<D, W>(a.ptr[pp], e);
-    for (int i = 0; i < pp; ++i) st_fin<D, W>(rp[i], e, g);
+    if (!have) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) g[l] = ld_in<D, W>(a.ptr[pp], e[l]);
+    }
+    for (int i = 0; i < pp; ++i) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(rp[i], e[l], g[l]);
+    }
   }
 }
 
@@ -293,22 +348,28 @@ __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
   return sd.nbig + (int)((u - big) / (uint32_t)sd.qbase);
 }
 
-template <class D, int W>
+template <class D, int W, int L, int B>
 __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const SegDesc &sd,
-                                          bool p2p, int64_t e) {
+                                          bool p2p, const int64_t (&e)[L]) {
   if (p2p) {
-    p2p_lane<D, W>(a, rp, e);
+    p2p_lane<D, W, L, B>(a, rp, e);
   } else {
-    const int j = section_of(sd, (e - sd.ring_begin) / kQuantum);
-    ring_lane<D, W>(a, rp, sd, j, e);
+    int j[L];
+#pragma unroll
+    for (int l = 0; l < L; ++l) j[l] = section_of(sd, (e[l] - sd.ring_begin) / kQuantum);
+    ring_lane<D, W, L, B>(a, rp, sd, j, e);
   }
 }
 
 // W elements per lane access: 16 bytes when every rank buffer is 16-byte
-// aligned, else 1 element.  Elements of a tile past a whole vector (only at
-// the end of the rank vectors) go one by one.
-template <class D, int W>
-__global__ __launch_bounds__(kThreads, OPTCC_MIN_WAVES) void optcc_exec_kernel(KArgs a) {
+// aligned, else 1 element.  A lane takes L such vectors of a tile
+// at a stride of one workgroup-width, in lockstep; vectors past the tile's
+// last whole group go one at a time, and elements past the last whole vector
+// (only at the end of the rank vectors) one by one.
+template <class D, int W, int L>
+__global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
+  constexpr int B = kHopWindow;
+  constexpr int64_t kStride = (int64_t)kThreads * W;
   __shared__ void *rp[kMaxRanks];
   for (int i = threadIdx.x; i < a.pp; i += kThreads) rp[i] = a.ptr[i];
   __syncthreads();
@@ -317,23 +378,43 @@ __global__ __launch_bounds__(kThreads, OPTCC_MIN_WAVES) void optcc_exec_kernel(K
     const bool p2p = td.meta & 1;
     const SegDesc sd = a.segs[td.meta >> 1];
     const int64_t end = td.begin + td.len;
-    for (int64_t e = td.begin + (int64_t)threadIdx.x * W; e < end; e += (int64_t)kThreads * W) {
-      if (e + W <= end) {
-        run_elems<D, W>(a, rp, sd, p2p, e);
+    int64_t e0 = td.begin + (int64_t)threadIdx.x * W;
+    for (; e0 + (L - 1) * kStride + W <= end; e0 += L * kStride) {
+      int64_t e[L];
+#pragma unroll
+      for (int l = 0; l < L; ++l) e[l] = e0 + l * kStride;
+      run_elems<D, W, L, B>(a, rp, sd, p2p, e);
+    }
+    for (; e0 < end; e0 += kStride) {
+      if (e0 + W <= end) {
+        const int64_t e[1] = {e0};
+        run_elems<D, W, 1, B>(a, rp, sd, p2p, e);
       } else {
-        for (int64_t x = e; x < end; ++x) run_elems<D, 1>(a, rp, sd, p2p, x);
+        for (int64_t x = e0; x < end; ++x) {
+          const int64_t e[1] = {x};
+          run_elems<D, 1, 1, B>(a, rp, sd, p2p, e);
+        }
       }
     }
   }
 }
 
 template <class D>
-hipError_t launch(const KArgs &a, bool vec16, hipStream_t st) {
+hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   constexpr int W16 = 16 / (int)sizeof(typename D::S);
   const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
-  if (vec16) hipLaunchKernelGGL((optcc_exec_kernel<D, W16>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((optcc_exec_kernel<D, 1>), grid, block, 0, st, a);
+  if (!vec16) {
+    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1>), grid, block, 0, st, a);
+    return hipGetLastError();
+  }
+  if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
+    if (two) {
+      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -424,15 +505,16 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
   for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool two = pl->pp <= kTwoVectorMaxHealthy;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
     a.se = launches == 1 ? se : sb + l + 1;
     hipError_t err = hipSuccess;
     switch (dtype) {
-      case OPTCC_F32: err = launch<F32>(a, vec16, st); break;
-      case OPTCC_BF16: err = launch<BF16>(a, vec16, st); break;
-      default: err = launch<I32>(a, vec16, st); break;
+      case OPTCC_F32: err = launch<F32>(a, vec16, two, st); break;
+      case OPTCC_BF16: err = launch<BF16>(a, vec16, false, st); break;
+      default: err = launch<I32>(a, vec16, two, st); break;
     }
     if (err != hipSuccess)
       return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));
