@@ -19,11 +19,16 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "achieved HBM GB/s of OptCC schedule execution (1 GPU) and % of peak BW"
 PEAK_GBPS = 8000.0  # MI355X HBM3E
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_01680_amd", "csrc", "optcc_exec.hip")
+# device code of the executor (kernels and the tile/segment table layouts)
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01680_amd", "csrc", f)
+               for f in ("optcc_kernels.hpp", "optcc_internal.hpp")]
 
 
 def kernel_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str, launches: int):

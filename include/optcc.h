@@ -93,7 +93,9 @@ void optcc_plan_free(optcc_plan_t *plan);
  *
  * Every step writes its destination rank's buffer; a partial sum that the
  * next step of the same section consumes is kept in registers.  The result is
- * bitwise deterministic.  Errors: OPTCC_EINVAL (mismatch with the plan, NULL
+ * bitwise deterministic.  With N = 0 (or an empty slot range) nothing is
+ * read or written and the pointers are not inspected.  Errors: OPTCC_EINVAL
+ * (mismatch with the plan, NULL
  * or misaligned pointers, overlapping buffers), OPTCC_EUNSUPPORTED
  * (p > OPTCC_MAX_EMULATE_RANKS), OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the
  * plan on a device allocates its tables).
@@ -184,10 +186,13 @@ int64_t optcc_plan_num_flows(const optcc_plan_t *plan);
 int64_t optcc_plan_get_flows(const optcc_plan_t *plan, optcc_flow_t *out, int64_t cap);
 
 /*
- * Algorithmic HBM bytes of one emulation call over [slot_begin, slot_end)
- * with `launches` as above: every load the executor must issue (each input
- * value once, plus the state a launch starts from) and every step's
- * destination write.  Writes: optcc counts each step write once.
+ * optcc_plan_traffic - algorithmic HBM bytes of one emulation call over
+ * [slot_begin, slot_end) with `launches` as above, for `dtype`: the loads the
+ * executor issues (each input value once, plus, per launch, the state the
+ * launch starts from) into *read_bytes and one write per step into
+ * *write_bytes.  Partial sums a step hands to the next step of the same
+ * section inside one launch stay in registers and are not counted as reads.
+ * Errors: OPTCC_EINVAL (NULL pointers, unknown dtype, bad slot range).
  */
 int optcc_plan_traffic(const optcc_plan_t *plan, optcc_dtype_t dtype, int slot_begin,
                        int slot_end, int launches, int64_t *read_bytes,

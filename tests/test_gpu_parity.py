@@ -44,6 +44,10 @@ PROFILES = [
     (3, {}), (3, {2: 0.5}), (4, {3: 0.5}), (5, {0: 0.5}), (5, {2: 0.75}), (8, {7: 0.875}),
     (8, {3: 0.25}), (6, {0: 0.5, 5: 0.75}), (9, {0: 0.875, 3: 0.75, 8: 0.5}), (16, {15: 0.5}),
     (12, {}), (20, {1: 0.5, 2: 0.5, 19: 0.9}), (40, {5: 0.6}),
+    # degenerate profiles: two healthy ranks, slowdown barely above 1, just
+    # under and exactly at l = 2
+    (4, {0: 0.5, 1: 0.75}), (5, {1: 0.5, 2: 0.5, 3: 0.5}), (8, {2: 0.9999999}),
+    (6, {5: 0.50000001}), (6, {5: 0.5}),
 ]
 # sizes span several 2048-element tiles, ragged tails, empty sections
 SIZES = [(1, 4), (37, 4), (64, 4), (1000, 8), (2048 * 3 + 64 * 5 + 3, 8), (40000, 12)]
@@ -192,3 +196,54 @@ def test_workload_full_size(o, name):
     del x0
     got_all = to_host(x, w.dtype)
     assert bits_equal(got_all, full)
+
+
+@pytest.mark.parametrize("dtype", ["i32", "f32"])
+def test_replanning_between_calls(o, dtype):
+    """Re-planning online (Sec. 4.3, schedule generation: closed-form rules,
+    cheap enough to run when a failure is detected): a sequence of NIC-loss
+    profiles on p=8 (PXN pooling: losing c of 8 NICs leaves bandwidth
+    (8-c)/8, Sec. 2), one fresh plan per call on the same buffers, each
+    result bit-exact against the oracle."""
+    p, n, k = 8, 300000, 16
+    seq = [{}, {3: 7 / 8}, {3: 6 / 8, 6: 7 / 8}, {3: 4 / 8}, {3: 2 / 8, 5: 4 / 8, 6: 6 / 8},
+           {0: 7 / 8, 1: 7 / 8, 2: 7 / 8, 4: 7 / 8}, {}]
+    x = rand_inputs(dtype, p, n, 77)
+    d = to_device(x, dtype)
+    d0 = d.clone()
+    prev = None
+    for slow in seq:
+        bw = _bw(p, slow)
+        _say(f"case replan dtype={dtype} slow={slow}")
+        pl = o.optcc_plan(p, bw, n, k)
+        d.copy_(d0)
+        o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+        torch.cuda.synchronize()
+        ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+        assert bits_equal(to_host(d, dtype), ref)
+        if prev is not None:
+            o.optcc_plan_free(prev)  # the previous plan's device tables go with it
+        prev = pl
+
+
+def test_largest_rank_count(o):
+    """p = OPTCC_MAX_EMULATE_RANKS (256): every rank pointer in the kernel
+    arguments; one past the limit is rejected before any launch."""
+    p, n, k = o.OPTCC_MAX_EMULATE_RANKS, 20000, 8
+    for dtype in ("i32", "f32"):
+        _say(f"case p=256 dtype={dtype}")
+        x, ref, got = _run_both(o, p, {0: 0.5, 100: 0.875, 255: 0.75}, n, k, dtype, seed=256)
+        assert bits_equal(got, ref)
+    big = o.optcc_plan(p + 1, [1.0] * (p + 1), 128, 4)
+    d = torch.zeros((p + 1, 128), dtype=torch.float32, device="cuda:0")
+    with pytest.raises(o.OptccError) as e:
+        o.optcc_allreduce_emulate(d, p + 1, 128, "f32", big)
+    assert e.value.status == o.OPTCC_EUNSUPPORTED
+
+
+def test_empty_vector(o):
+    """N = 0: a valid plan with empty segments; emulation is a no-op."""
+    pl = o.optcc_plan(5, [1, 1, 0.5, 1, 1], 0, 8)
+    d = torch.zeros((5, 0), dtype=torch.float32, device="cuda:0")
+    o.optcc_allreduce_emulate(d, 5, 0, "f32", pl)
+    torch.cuda.synchronize()

@@ -37,6 +37,8 @@ PROFILES = [
     (8, {7: 0.875}), (8, {0: 0.25}), (9, {4: 0.5, 5: 0.5}), (6, {0: 0.5, 5: 0.75}),
     (9, {0: 0.875, 3: 0.75, 8: 0.5}), (16, {15: 0.5}), (12, {}), (10, {3: 0.5000001}),
     (6, {1: 0.9, 2: 0.8, 3: 0.7, 4: 0.6}),
+    (4, {0: 0.5, 1: 0.75}), (5, {1: 0.5, 2: 0.5, 3: 0.5}), (8, {2: 0.9999999}),
+    (6, {5: 0.50000001}), (6, {5: 0.5}), (256, {0: 0.5, 100: 0.875, 255: 0.75}),
 ]
 SIZES = [(0, 4), (1, 4), (63, 4), (64, 4), (257, 8), (1000, 4), (64 * 53 + 9, 8), (5000, 12)]
 
@@ -162,6 +164,8 @@ def test_errors(o):
     assert L.optcc_allreduce_emulate_slots(ptrs, 4, 100, 0, pl.handle, 2, 2, 1, None) == 0
     pl0 = o.optcc_plan(4, [1, 1, 1, 0.5], 0, 4)
     assert L.optcc_allreduce_emulate(ptrs, 4, 0, 0, pl0.handle, None) == 0
+    nulls = (ctypes.c_void_p * 4)(0, 0, 0, 0)
+    assert L.optcc_allreduce_emulate(nulls, 4, 0, 0, pl0.handle, None) == 0
 
 
 def test_exports_match_header(o):
