@@ -17,7 +17,10 @@
  *     the caller (optcc_plan / optcc_plan_free); it lazily owns one small
  *     read-only device copy of its step tables per device it has run on.
  *   - "stream" is a hipStream_t (NULL = the default stream).  Emulation calls
- *     are asynchronous and return once the kernels are enqueued.
+ *     are asynchronous and return once the kernels are enqueued.  The first
+ *     call of a plan on a device uploads its tables (hipMalloc + hipMemcpy);
+ *     every later call only launches kernels and may be captured in a HIP
+ *     graph.
  */
 #ifndef OPTCC_H
 #define OPTCC_H

@@ -247,3 +247,39 @@ def test_empty_vector(o):
     d = torch.zeros((5, 0), dtype=torch.float32, device="cuda:0")
     o.optcc_allreduce_emulate(d, 5, 0, "f32", pl)
     torch.cuda.synchronize()
+
+
+def test_graph_capture_replays(o):
+    """After its first call on a device (which uploads the plan tables) an
+    AllReduce is one kernel launch, so it can be captured in a HIP graph.
+    Each replay, with eager restores and synchronisations in between, equals
+    the eager result bit for bit."""
+    p, n, k = 8, 200000, 16
+    bw = _bw(p, {7: 0.875})
+    pl = o.optcc_plan(p, bw, n, k)
+    for dtype in ("f32", "bf16", "i32"):
+        x = rand_inputs(dtype, p, n, 31)
+        d = to_device(x, dtype)
+        d0 = d.clone()
+        o.optcc_allreduce_emulate(d, p, n, dtype, pl)  # first use: table upload
+        torch.cuda.synchronize()
+        eager = d.clone()
+        ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+        assert bits_equal(to_host(eager, dtype), ref)
+        g = torch.cuda.CUDAGraph()
+        d.copy_(d0)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+        torch.cuda.synchronize()
+        for rep in range(4):
+            _say(f"case graph replay dtype={dtype} rep={rep}")
+            d.copy_(d0)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(d.view(torch.int16 if dtype == "bf16" else torch.int32),
+                               eager.view(torch.int16 if dtype == "bf16" else torch.int32))
+        del g
