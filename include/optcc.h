@@ -201,6 +201,27 @@ int optcc_plan_traffic(const optcc_plan_t *plan, optcc_dtype_t dtype, int slot_b
                        int slot_end, int launches, int64_t *read_bytes,
                        int64_t *write_bytes);
 
+/*
+ * optcc_plan_timeline - evaluate the plan's schedule in the paper's network
+ * model: start and finish time of every flow (in optcc_plan_get_flows order)
+ * and the makespan, in the unit of optcc_model_time.
+ *   - every rank has one send and one receive port, each carrying one flow at
+ *     a time (Sec. 4.1: a NIC receives at most one flow at a time; Sec. 4.2:
+ *     no NIC sends or receives two flows at once; full duplex);
+ *   - a flow of len elements between ranks a and b lasts len * max(l_a, l_b)
+ *     (Sec. 3 model with the time weighting of App. B.1);
+ *   - a flow starts after the earlier steps of its section that wrote its
+ *     source's or its destination's range have finished (Sec. 3: a rank sends
+ *     only data it holds);
+ *   - work-conserving list scheduling in flow order.
+ * The paper's own slot-level overlay of patterns A-D is given only as
+ * figures; this is an evaluation of the same flows under the same rules.
+ * start/finish may be NULL when cap = 0.  Errors: OPTCC_EINVAL,
+ * OPTCC_EUNSUPPORTED (more than 2^26 flows), OPTCC_ENOMEM.
+ */
+int optcc_plan_timeline(const optcc_plan_t *plan, double *start, double *finish, int64_t cap,
+                        double *makespan);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,0 +1,127 @@
+"""Evaluated schedule of the oracle's flows in the paper's network model.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Rules (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
+* Sec. 3 model: a healthy NIC moves one element per time unit, a NIC with
+  slowdown l one element per l units; App. B.1 time weighting: a transfer that
+  touches a slow NIC costs the slow rate on both ends, so a flow of len
+  elements between ranks a and b lasts len * max(l_a, l_b).
+* Sec. 4.1: each NIC receives at most one flow at a time; Sec. 4.2: no NIC
+  sends or receives two flows at once; the straggler sends and receives at
+  the same time (full duplex).  So every rank has one send and one receive
+  port, each busy with at most one flow.
+* Sec. 3 correctness (i): a rank transmits only data it already holds: a
+  flow waits for the earlier steps of its section that wrote its source's or
+  its destination's range.
+* Scheduling policy (this build's reading, the pattern figures being
+  missing): non-preemptive, work-conserving list scheduling in the serial
+  step order; at every event time the unstarted flows are scanned in that
+  order and each one whose dependencies are done and whose two ports are free
+  starts.
+
+Times are exact rationals (``fractions.Fraction``), so there are no ties to
+break by tolerance (the library, in doubles, merges events closer than 1e-9 of
+the current time).  The naive scan is quadratic: small schedules only.
+"""
+from __future__ import annotations
+
+from fractions import Fraction as F
+
+
+def slowdowns(bandwidths):
+    """l_i = max(b)/b_i, read as the nearest fraction with denominator at most
+    10**6: bandwidths are NIC fractions (7/8, 2/3, ...) given as doubles, so
+    2/3 means l = 3/2 and simultaneous events stay simultaneous."""
+    b = [F(x) for x in bandwidths]
+    bmax = max(b)
+    return [(bmax / x).limit_denominator(10**6) for x in b]
+
+
+def dependencies(steps):
+    """For every step, the earlier steps of its section that last wrote one of
+    its sources or its destination."""
+    last = {}
+    deps = []
+    for i, st in enumerate(steps):
+        sec = (st["seg"], st["sec"])
+        d = set()
+        for r in list(st["srcs"]) + [st["dst"]]:
+            if (r, sec) in last:
+                d.add(last[(r, sec)])
+        deps.append(d)
+        last[(st["dst"], sec)] = i
+    return deps
+
+
+def evaluate(sched, bandwidths):
+    """(makespan, [(start, finish) per flow in flow order])."""
+    steps = sched.steps()
+    ell = slowdowns(bandwidths)
+    deps = dependencies(steps)
+    flows = []
+    for i, st in enumerate(steps):
+        for src in st["srcs"]:
+            flows.append((i, src, st["dst"], st["len"] * max(ell[src], ell[st["dst"]])))
+    left = [len(st["srcs"]) for st in steps]
+    done_steps = set()
+    start = [None] * len(flows)
+    finish = [None] * len(flows)
+    send_free = [F(0)] * sched.p
+    recv_free = [F(0)] * sched.p
+    t = F(0)
+    running = []
+    remaining = len(flows)
+    while remaining:
+        for f, (i, a, b, dur) in enumerate(flows):
+            if start[f] is not None or not deps[i] <= done_steps:
+                continue
+            if send_free[a] > t or recv_free[b] > t:
+                continue
+            start[f], finish[f] = t, t + dur
+            send_free[a] = recv_free[b] = t + dur
+            running.append(f)
+        if not running:
+            raise RuntimeError("no flow can start")
+        t = min(finish[f] for f in running)
+        for f in [f for f in running if finish[f] == t]:
+            running.remove(f)
+            remaining -= 1
+            i = flows[f][0]
+            left[i] -= 1
+            if left[i] == 0:
+                done_steps.add(i)
+    return max(finish, default=F(0)), list(zip(start, finish))
+
+
+def validate(sched, bandwidths, times):
+    """Check a timeline against the model, whatever policy produced it:
+    durations, one flow per port at a time, and data dependencies.
+    Returns a list of violations (empty when valid)."""
+    steps = sched.steps()
+    ell = slowdowns(bandwidths)
+    deps = dependencies(steps)
+    errs = []
+    flows = [(i, src, st["dst"], st["len"]) for i, st in enumerate(steps) for src in st["srcs"]]
+    if len(flows) != len(times):
+        return [f"{len(times)} times for {len(flows)} flows"]
+    step_end = {}
+    for (i, a, b, ln), (s, e) in zip(flows, times):
+        dur = ln * max(ell[a], ell[b])
+        if abs(F(e) - F(s) - dur) > F(1, 10**6) * max(1, dur):
+            errs.append(f"flow of step {i}: duration {e - s} != {dur}")
+        step_end[i] = max(step_end.get(i, F(-1)), F(e))
+    for port in ("send", "recv"):
+        busy = {}
+        for (i, a, b, ln), (s, e) in zip(flows, times):
+            busy.setdefault(a if port == "send" else b, []).append((F(s), F(e)))
+        for r, iv in busy.items():
+            iv.sort()
+            for (s0, e0), (s1, e1) in zip(iv, iv[1:]):
+                if s1 < e0 - F(1, 10**6) * max(1, e0):
+                    errs.append(f"rank {r} {port} port: overlapping flows at {s1}")
+    for (i, a, b, ln), (s, e) in zip(flows, times):
+        for d in deps[i]:
+            if F(s) < step_end[d] - F(1, 10**6) * max(1, step_end[d]):
+                errs.append(f"step {i} starts before its dependency {d} ends")
+    return errs

@@ -7,7 +7,10 @@
 #include <cmath>
 #include <cstring>
 #include <new>
+#include <queue>
+#include <set>
 #include <string>
+#include <unordered_map>
 
 #include "optcc_internal.hpp"
 
@@ -421,5 +424,148 @@ extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, i
   }
   *rd = r * es;
   *wr = w * es;
+  return OPTCC_OK;
+}
+
+// ------------------------------------------------------------- timeline
+// Evaluation of the plan's flows in the paper's network model (Sec. 3 model;
+// Sec. 4.1 flow rule; App. B.1 time weighting):
+//  * every rank has a send port and a receive port (full duplex), each
+//    carrying at most one flow at a time;
+//  * a flow of len elements between ranks a and b lasts len * max(l_a, l_b);
+//  * a flow starts only after every earlier step of its section that wrote
+//    its source's range, or its destination's range, has finished (a rank
+//    sends only data it holds); a step finishes with its last flow;
+//  * list scheduling: whenever ports free up, ready flows are started in
+//    flow order (slot, segment, section, hop) if both their ports are free.
+// Times are doubles; events closer than 1e-9 of the current time are merged.
+extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double *finish,
+                                   int64_t cap, double *makespan) {
+  if (!pl || !makespan) return fail(OPTCC_EINVAL, "plan and makespan must be non-NULL");
+  if (cap > 0 && (!start || !finish)) return fail(OPTCC_EINVAL, "start/finish are NULL");
+  if (pl->num_flows > ((int64_t)1 << 26))
+    return fail(OPTCC_EUNSUPPORTED, "timeline limited to 2^26 flows");
+  try {
+    // steps and flows in execution order
+    std::vector<int32_t> st_dst, f_src;
+    std::vector<int64_t> st_first, f_step;
+    std::vector<double> f_dur;
+    std::vector<std::vector<int64_t>> deps;
+    std::unordered_map<uint64_t, int64_t> last_writer;  // (rank, seg, sec) -> step
+    auto key = [](int rank, int seg, int sec) {
+      return ((uint64_t)(uint32_t)rank << 40) | ((uint64_t)(uint32_t)seg << 12) | (uint64_t)(sec + 1);
+    };
+    for_each_step(*pl, [&](int, int g, int sec, int, int dst, const int *srcs, int ns,
+                           int64_t, int64_t len) {
+      const int64_t sid = (int64_t)st_dst.size();
+      st_dst.push_back(dst);
+      st_first.push_back((int64_t)f_src.size());
+      std::vector<int64_t> d;
+      auto dep = [&](int rank) {
+        auto it = last_writer.find(key(rank, g, sec));
+        if (it != last_writer.end() && std::find(d.begin(), d.end(), it->second) == d.end())
+          d.push_back(it->second);
+      };
+      for (int i = 0; i < ns; ++i) dep(srcs[i]);
+      dep(dst);
+      deps.push_back(std::move(d));
+      for (int i = 0; i < ns; ++i) {
+        f_src.push_back(srcs[i]);
+        f_step.push_back(sid);
+        f_dur.push_back((double)len * std::max(pl->ell[(size_t)srcs[i]], pl->ell[(size_t)dst]));
+      }
+      last_writer[key(dst, g, sec)] = sid;
+    });
+    st_first.push_back((int64_t)f_src.size());
+    const int64_t nst = (int64_t)st_dst.size(), nfl = (int64_t)f_src.size();
+    std::vector<int32_t> pending((size_t)nst), left((size_t)nst);
+    std::vector<std::vector<int64_t>> dependents((size_t)nst);
+    for (int64_t s = 0; s < nst; ++s) {
+      pending[(size_t)s] = (int32_t)deps[(size_t)s].size();
+      left[(size_t)s] = (int32_t)(st_first[(size_t)s + 1] - st_first[(size_t)s]);
+      for (int64_t d : deps[(size_t)s]) dependents[(size_t)d].push_back(s);
+    }
+    const int p = pl->p;
+    std::vector<double> fs((size_t)nfl, -1.0), ff((size_t)nfl, -1.0);
+    std::vector<char> send_busy((size_t)p, 0), recv_busy((size_t)p, 0);
+    // Ready flows by (sender, receiver).  Flows of one pair share both ports,
+    // so only the earliest of them in flow order can be the next to start.
+    std::vector<std::unordered_map<int, std::set<int64_t>>> out_ready((size_t)p);
+    std::vector<std::set<int>> in_partners((size_t)p);
+    using Ev = std::pair<double, int64_t>;
+    std::priority_queue<Ev, std::vector<Ev>, std::greater<Ev>> ev;
+    std::vector<int64_t> cand;
+    std::vector<int> freed_send, freed_recv;
+    auto make_ready = [&](int64_t s) {
+      const int b = st_dst[(size_t)s];
+      for (int64_t f = st_first[(size_t)s]; f < st_first[(size_t)s + 1]; ++f) {
+        const int a = f_src[(size_t)f];
+        out_ready[(size_t)a][b].insert(f);
+        in_partners[(size_t)b].insert(a);
+        cand.push_back(f);
+      }
+    };
+    for (int64_t s = 0; s < nst; ++s)
+      if (pending[(size_t)s] == 0) make_ready(s);
+    double t = 0.0, last = 0.0;
+    int64_t done = 0;
+    while (done < nfl) {
+      // candidates: newly ready flows and the head of every ready pair that
+      // touches a port freed at t; start them in flow order
+      for (int a : freed_send)
+        for (auto &kv : out_ready[(size_t)a])
+          if (!recv_busy[(size_t)kv.first]) cand.push_back(*kv.second.begin());
+      for (int b : freed_recv)
+        for (int a : in_partners[(size_t)b])
+          if (!send_busy[(size_t)a]) cand.push_back(*out_ready[(size_t)a][b].begin());
+      freed_send.clear();
+      freed_recv.clear();
+      std::sort(cand.begin(), cand.end());
+      cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
+      for (int64_t f : cand) {
+        if (fs[(size_t)f] >= 0.0) continue;
+        const int a = f_src[(size_t)f], b = st_dst[(size_t)f_step[(size_t)f]];
+        if (send_busy[(size_t)a] || recv_busy[(size_t)b]) continue;
+        auto &q = out_ready[(size_t)a][b];
+        if (q.empty() || *q.begin() != f) continue;  // an earlier flow of the pair is waiting
+        fs[(size_t)f] = t;
+        ff[(size_t)f] = t + f_dur[(size_t)f];
+        send_busy[(size_t)a] = 1;
+        recv_busy[(size_t)b] = 1;
+        q.erase(q.begin());
+        if (q.empty()) {
+          out_ready[(size_t)a].erase(b);
+          in_partners[(size_t)b].erase(a);
+        }
+        ev.push({ff[(size_t)f], f});
+      }
+      cand.clear();
+      if (ev.empty()) return fail(OPTCC_EINVAL, "timeline: no flow can start (dependency cycle)");
+      t = ev.top().first;
+      const double tol = 1e-9 * std::max(1.0, t);
+      while (!ev.empty() && ev.top().first <= t + tol) {
+        const int64_t f = ev.top().second;
+        ev.pop();
+        ++done;
+        last = std::max(last, ff[(size_t)f]);
+        const int a = f_src[(size_t)f], b = st_dst[(size_t)f_step[(size_t)f]];
+        send_busy[(size_t)a] = 0;
+        recv_busy[(size_t)b] = 0;
+        freed_send.push_back(a);
+        freed_recv.push_back(b);
+        const int64_t s = f_step[(size_t)f];
+        if (--left[(size_t)s] == 0)
+          for (int64_t d : dependents[(size_t)s])
+            if (--pending[(size_t)d] == 0) make_ready(d);
+      }
+    }
+    for (int64_t f = 0; f < std::min(cap, nfl); ++f) {
+      start[f] = fs[(size_t)f];
+      finish[f] = ff[(size_t)f];
+    }
+    *makespan = last;
+  } catch (const std::bad_alloc &) {
+    return fail(OPTCC_ENOMEM, "out of host memory");
+  }
   return OPTCC_OK;
 }

@@ -25,7 +25,8 @@ KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi"}
 EXPORTED = ("optcc_plan", "optcc_plan_free", "optcc_allreduce_emulate",
             "optcc_allreduce_emulate_slots", "optcc_model_time", "optcc_lower_bound",
             "optcc_last_error", "optcc_plan_info", "optcc_plan_segments",
-            "optcc_plan_num_flows", "optcc_plan_get_flows", "optcc_plan_traffic")
+            "optcc_plan_num_flows", "optcc_plan_get_flows", "optcc_plan_traffic",
+            "optcc_plan_timeline")
 
 
 class PlanInfo(ctypes.Structure):
@@ -76,6 +77,8 @@ def _load():
     L.optcc_plan_traffic.argtypes = [vp, i32, i32, i32, i32, ctypes.POINTER(i64),
                                      ctypes.POINTER(i64)]
     L.optcc_plan_traffic.restype = i32
+    L.optcc_plan_timeline.argtypes = [vp, vp, vp, i64, ctypes.POINTER(dbl)]
+    L.optcc_plan_timeline.restype = i32
     return L
 
 
@@ -146,6 +149,16 @@ class Plan:
         _check(_lib.optcc_plan_traffic(self._h, DTYPES[dtype], slot_begin, slot_end, launches,
                                        ctypes.byref(r), ctypes.byref(w)))
         return r.value, w.value
+
+    def timeline(self, with_flows=True):
+        """(makespan, start[], finish[]) of the evaluated schedule."""
+        n = self.num_flows if with_flows else 0
+        st = np.zeros(max(n, 1), np.float64)
+        fi = np.zeros(max(n, 1), np.float64)
+        mk = ctypes.c_double()
+        _check(_lib.optcc_plan_timeline(self._h, st.ctypes.data, fi.ctypes.data, n,
+                                        ctypes.byref(mk)))
+        return mk.value, st[:n], fi[:n]
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -234,3 +247,7 @@ def optcc_lower_bound(p: int, link_bandwidths, N: int) -> float:
     if math.isnan(t):
         raise OptccError(OPTCC_EINVAL, optcc_last_error())
     return t
+
+
+def optcc_plan_timeline(plan: Plan):
+    return plan.timeline()

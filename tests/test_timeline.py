@@ -1,0 +1,111 @@
+"""Evaluated schedule (the plan's flows timed in the paper's network model).
+
+The library's timeline must equal the oracle's exact-rational evaluation of
+the same rules flow by flow, and pass the oracle's policy-free validator.
+The validator itself is checked by planting mistakes in a valid timeline.
+"""
+from fractions import Fraction as F
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import model
+from oracle import timeline as T
+
+
+@pytest.fixture(scope="module")
+def o():
+    from paper_2606_01680_amd import optcc
+    return optcc
+
+
+def _bw(p, slow):
+    b = [1.0] * p
+    for r, v in slow.items():
+        b[r] = v
+    return b
+
+
+CASES = [
+    (3, {}, 3 * 64 * 4, 4), (7, {}, 7 * 64 * 8, 8), (4, {3: 0.5}, 5000, 8), (5, {0: 0.5}, 64 * 4 * 4 * 8, 4),
+    (5, {0: 2 / 3}, 52 * 64 * 4, 4), (6, {2: 0.75}, 3000, 4), (8, {7: 0.875}, 64 * 7 * 8 * 4, 8),
+    (7, {0: 0.5, 1: 0.75}, 64 * 5 * 8 * 4, 8), (9, {0: 0.875, 3: 0.75, 8: 0.5}, 4000, 4),
+    (6, {5: 0.25}, 64 * 5 * 4, 4),
+]
+
+
+@pytest.mark.parametrize("p,slow,n,k", CASES)
+def test_timeline_equals_oracle(o, p, slow, n, k):
+    bw = _bw(p, slow)
+    sched = oracle.Schedule(p, bw, n, k)
+    mk_ref, ref = T.evaluate(sched, bw)
+    pl = o.optcc_plan(p, bw, n, k)
+    mk, st, fi = pl.timeline()
+    scale = max(1.0, float(mk_ref))
+    assert abs(mk - float(mk_ref)) <= 1e-9 * scale
+    assert len(st) == len(ref)
+    assert np.allclose(st, [float(a) for a, _ in ref], rtol=0, atol=1e-9 * scale)
+    assert np.allclose(fi, [float(b) for _, b in ref], rtol=0, atol=1e-9 * scale)
+    assert T.validate(sched, bw, list(zip(st, fi))) == []
+
+
+@pytest.mark.parametrize("p,slow,n,k", CASES)
+def test_evaluated_respects_lower_bound(p, slow, n, k):
+    """Theorems 1/2 and the tight bound hold for any correct AllReduce, so
+    also for this evaluated schedule."""
+    bw = _bw(p, slow)
+    mk, _ = T.evaluate(oracle.Schedule(p, bw, n, k), bw)
+    assert mk >= model.lower_bound(bw, n)
+
+
+@pytest.mark.parametrize("p", [3, 4, 7, 9])
+def test_ring_attains_t0(p):
+    """Sec. 3: without stragglers the ring reaches T0 = 2(p-1)n/p exactly when
+    every section has the same size."""
+    k = 4
+    n = p * 64 * k * 3
+    bw = [1.0] * p
+    mk, _ = T.evaluate(oracle.Schedule(p, bw, n, k), bw)
+    assert mk == model.t0(p, n)
+
+
+def test_validator_catches_planted_mistakes():
+    """The validator rejects a shortened flow, two flows on one port at once,
+    and a flow that starts before the data it forwards exists."""
+    p, bw, n, k = 5, [0.5, 1, 1, 1, 1], 64 * 4 * 4, 4
+    sched = oracle.Schedule(p, bw, n, k)
+    _, good = T.evaluate(sched, bw)
+    assert T.validate(sched, bw, good) == []
+    flows = [(st["slot"], src, st["dst"]) for st in sched.steps() for src in st["srcs"]]
+    # shorten the first flow
+    bad = list(good)
+    s, e = bad[0]
+    bad[0] = (s, s + (e - s) / 2)
+    assert any("duration" in x for x in T.validate(sched, bw, bad))
+    # move a Stage-4 hop to time 0: its data does not exist yet, and its
+    # ports are busy with Stage-1 flows
+    i = next(i for i, f in enumerate(flows) if f[0] == 4)
+    s, e = good[i]
+    bad = list(good)
+    bad[i] = (F(0), e - s)
+    errs = T.validate(sched, bw, bad)
+    assert any("dependency" in x for x in errs) and any("overlapping" in x for x in errs)
+
+
+@pytest.mark.parametrize("w", ["p4_f32", "p8_f32", "p16_bf16"])
+def test_workload_evaluated_times(o, w):
+    """Full-size evaluated makespans against the closed forms and bounds:
+    p4 and p16 (l = 2) at or below (k+1)/k l n, p8 (bubble filling) within
+    1 % of its closed form; always above the best lower bound."""
+    from paper_2606_01680_amd.workloads import WORKLOADS
+    W = WORKLOADS[w]
+    pl = o.optcc_plan(W.p, W.bandwidths, W.n, W.k)
+    mk, _, _ = pl.timeline(with_flows=False)
+    closed = o.optcc_model_time(pl)
+    lb = o.optcc_lower_bound(W.p, W.bandwidths, W.n)
+    assert mk >= lb * (1 - 1e-12)
+    if pl.kind == "single_ge2":
+        assert mk <= closed * (1 + 1e-12)
+    else:
+        assert mk <= closed * 1.01
