@@ -122,7 +122,10 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
   for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   hipStream_t st = static_cast<hipStream_t>(stream);
+  // short chains: two vectors per lane and per-XCD tile runs (both measured
+  // faster up to 32 healthy ranks and neutral or slower beyond)
   const bool two = pl->pp <= kTwoVectorMaxHealthy;
+  a.xcd_runs = pl->pp <= kTwoVectorMaxHealthy ? 1 : 0;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;

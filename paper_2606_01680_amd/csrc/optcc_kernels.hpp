@@ -61,6 +61,7 @@ struct KArgs {
   int64_t n;
   int32_t pp, m;
   int32_t sb, se;  // slot range [sb, se)
+  int32_t xcd_runs;  // 1: each XCD takes a contiguous run of tiles
   // rank pointers: [0, pp) healthy ranks in ring order, [pp, pp+m) stragglers
   // sorted by slowdown (worst first)
   void *ptr[kMaxRanks];
@@ -373,7 +374,16 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
   __shared__ void *rp[kMaxRanks];
   for (int i = threadIdx.x; i < a.pp; i += kThreads) rp[i] = a.ptr[i];
   __syncthreads();
-  for (int64_t t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+  // Workgroups are dealt to the XCDs round robin by workgroup index.  With
+  // xcd_runs, workgroup t0 takes tile (t0 mod X) * per + t0 / X, so each XCD
+  // sweeps its own contiguous run of tiles.  Any XCD count keeps every tile
+  // covered exactly once; X = 8 matches MI355X.
+  constexpr int64_t kXcds = 8;
+  const int64_t per = (a.ntiles + kXcds - 1) / kXcds;
+  const int64_t cover = a.xcd_runs ? per * kXcds : a.ntiles;
+  for (int64_t t0 = blockIdx.x; t0 < cover; t0 += gridDim.x) {
+    const int64_t t = a.xcd_runs ? (t0 % kXcds) * per + t0 / kXcds : t0;
+    if (t >= a.ntiles) continue;
     const TileDesc td = a.tiles[t];
     const bool p2p = td.meta & 1;
     const SegDesc sd = a.segs[td.meta >> 1];
