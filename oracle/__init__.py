@@ -31,9 +31,10 @@ _LIB = os.path.join(_HERE, "liboptcc_oracle.so")
 
 DTYPES = {"f32": 0, "bf16": 1, "i32": 2}
 NP_DTYPES = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32}
-KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi"}
+KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi", 4: "servers"}
 COPY, REDUCE = 0, 1
-NUM_SLOTS = 6
+NUM_SLOTS = 6           # one GPU per server
+NUM_SERVER_SLOTS = 12   # several GPUs per server
 
 _lib = None
 
@@ -56,6 +57,8 @@ def lib():
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
         L.orc_build.argtypes = [i32, vp, i64, i32, i32, i32, ctypes.POINTER(vp)]
         L.orc_build.restype = i32
+        L.orc_build_servers.argtypes = [i32, i32, vp, i64, i32, i32, i32, ctypes.POINTER(vp)]
+        L.orc_build_servers.restype = i32
         L.orc_free.argtypes = [vp]
         L.orc_info.argtypes = [vp, vp, vp, vp, vp]
         L.orc_segments.argtypes = [vp, vp, vp, vp]
@@ -82,20 +85,29 @@ def _ptr(a: np.ndarray) -> int:
 
 class Schedule:
     """The oracle's own schedule for (p, bandwidths, N, k); optionally only
-    the steps of segments [seg_lo, seg_hi)."""
+    the steps of segments [seg_lo, seg_hi).  ``Schedule.servers`` builds the
+    several-GPUs-per-server schedule (App. E)."""
 
-    def __init__(self, p, bandwidths, n, k, seg_lo=0, seg_hi=0):
+    def __init__(self, p, bandwidths, n, k, seg_lo=0, seg_hi=0, _servers=None):
         L = lib()
         bw = np.ascontiguousarray(np.asarray(bandwidths, dtype=np.float64))
-        if bw.shape != (p,):
-            raise ValueError("need one bandwidth per rank")
         h = ctypes.c_void_p()
-        rc = L.orc_build(int(p), _ptr(bw), int(n), int(k), int(seg_lo), int(seg_hi),
-                         ctypes.byref(h))
+        if _servers is None:
+            if bw.shape != (p,):
+                raise ValueError("need one bandwidth per rank")
+            rc = L.orc_build(int(p), _ptr(bw), int(n), int(k), int(seg_lo), int(seg_hi),
+                             ctypes.byref(h))
+        else:
+            q, g = _servers
+            if bw.shape != (q,):
+                raise ValueError("need one bandwidth per server")
+            rc = L.orc_build_servers(int(q), int(g), _ptr(bw), int(n), int(k), int(seg_lo),
+                                     int(seg_hi), ctypes.byref(h))
+            p = q * g
         if rc != 0:
             raise OracleError(rc, L.orc_last_error().decode())
         self._h = h
-        info = np.zeros(8, np.int64)
+        info = np.zeros(12, np.int64)
         ring = np.zeros(max(p, 1), np.int32)
         strag = np.zeros(max(p, 1), np.int32)
         ell = np.zeros(p, np.float64)
@@ -104,14 +116,21 @@ class Schedule:
         self.kind = KINDS[int(info[3])]
         self.pp, self.n = int(info[4]), int(info[5])
         self.nsteps, self.npool = int(info[6]), int(info[7])
+        self.g, self.q, self.nseg = int(info[8]), int(info[9]), int(info[10])
+        self.num_slots = NUM_SERVER_SLOTS if self.g > 1 else NUM_SLOTS
         self.ring = ring[: self.pp].copy()
         self.stragglers = strag[: self.m].copy()
         self.ell = ell
-        off = np.zeros(self.k, np.int64)
-        ln = np.zeros(self.k, np.int64)
-        p2p = np.zeros(self.k, np.int64)
+        off = np.zeros(self.nseg, np.int64)
+        ln = np.zeros(self.nseg, np.int64)
+        p2p = np.zeros(self.nseg, np.int64)
         L.orc_segments(h, _ptr(off), _ptr(ln), _ptr(p2p))
         self.seg_off, self.seg_len, self.p2p_len = off, ln, p2p
+
+    @classmethod
+    def servers(cls, q, g, server_bandwidths, n, k, seg_lo=0, seg_hi=0):
+        """q servers of g GPUs (ranks server-major), one bandwidth per server."""
+        return cls(q * g, server_bandwidths, n, k, seg_lo, seg_hi, _servers=(q, g))
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -140,7 +159,7 @@ class Schedule:
                 for st in self.steps() for src in st["srcs"]]
 
 
-def run(sched: Schedule, dtype: str, bufs: np.ndarray, slot_lo=0, slot_hi=NUM_SLOTS):
+def run(sched: Schedule, dtype: str, bufs: np.ndarray, slot_lo=0, slot_hi=NUM_SERVER_SLOTS):
     """Execute the schedule in place on a C-contiguous [p, N] host array."""
     if not (bufs.flags.c_contiguous and bufs.shape == (sched.p, sched.n)
             and bufs.dtype == NP_DTYPES[dtype]):
@@ -153,7 +172,7 @@ def run(sched: Schedule, dtype: str, bufs: np.ndarray, slot_lo=0, slot_hi=NUM_SL
 
 
 def run_sampled(sched: Schedule, dtype: str, cols: np.ndarray, coords: np.ndarray,
-                slot_lo=0, slot_hi=NUM_SLOTS):
+                slot_lo=0, slot_hi=NUM_SERVER_SLOTS):
     """Execute the schedule at sorted coordinates only; cols is [p, S] and is
     updated in place."""
     coords = np.ascontiguousarray(coords, dtype=np.int64)

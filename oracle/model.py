@@ -104,3 +104,29 @@ def straggler_volume_optimum(p, ell, n):
     """z* n with z* = 2(p-1)/(l(p-2)+2): the straggler send/receive volume at
     the minimiser of the tight bound's min-max problem (App. B.1)."""
     return F(2 * (p - 1)) / (F(ell) * (p - 2) + 2) * n
+
+
+# ------------------------------------------------ several GPUs per server
+def t0_servers(p, g, n):
+    """Fault-free optimum with g GPUs per server: 2(p-1)n/(gp) (Sec. 3)."""
+    return F(2 * (p - 1), g * p) * n
+
+
+def optcc_servers(q, g, ell, n, k):
+    """App. E time analysis (single straggler server, no bubble filling):
+    T <= l n (k+5.5)/(g k) for l >= 2, 2 n (k+5.5)/(g k) for l < 2."""
+    ell = F(ell)
+    body = ell if ell >= 2 else F(2)
+    return body * n * (k + F(11, 2)) / (g * k)
+
+
+def lb_servers_weak(q, g, ell, n):
+    """Theorem 3: T >= (n/g) max{2l(q-1)/(1+l(q-1)), l} (App. B.3 form)."""
+    ell = F(ell)
+    return F(n, g) * max(2 * ell * (q - 1) / (1 + ell * (q - 1)), ell)
+
+
+def lb_servers_tight(q, g, ell, n):
+    """Tight multi-GPU bound (App. B.3): T >= (n/g) max{2l(q-1)/(l(q-2)+2), l}."""
+    ell = F(ell)
+    return F(n, g) * max(2 * ell * (q - 1) / (ell * (q - 2) + 2), ell)

@@ -44,6 +44,23 @@
  * segments never share coordinates, and within a section the slot order is
  * the section's own stage order.
  *
+ * Several GPUs per server (App. E): q servers of g GPUs, ranks numbered
+ * server-major (rank = server * g + local index); one bandwidth per server
+ * (PXN pools a server's NICs, Sec. 2).  The vector is split into g parts,
+ * part i led by local GPU i of every server; each part runs the schedule
+ * above among the leaders, with NVLink phases around the NIC stages:
+ * collect = a reduce chain along the server's local ring backwards onto the
+ * leader, distribute = a copy chain forwards from the leader.  Slots 0..11:
+ *   0 N3 collect at the straggler (type 2)   1 N1 collect at healthy servers
+ *   2 S3 straggler sum into the chain start (type 2)   3 S1 chain of leaders
+ *   4 S2 holder -> straggler leader, which adds its own value (type 1)
+ *   5 N2 fold: forward reduce chain on the straggler (type 1)
+ *   6 N3 copy back: backward copy chain on the straggler (type 1)
+ *   7 S3 straggler leader -> holder (type 1)   8 S4 allgather of leaders
+ *   9 N4 distribute on healthy servers   10 S2 holder -> straggler (type 2)
+ *   11 N2 distribute on the straggler (type 2)
+ * Patterns A, C use type 1 (S1-S2-S3-S4), B, D type 2 (S3-S1-S4-S2).
+ *
  * Build:  gcc -O2 -std=c99 -ffp-contract=off -fno-fast-math -shared -fPIC
  */
 #include <math.h>
@@ -63,6 +80,8 @@
 #define ORC_SINGLE_GE2 1 /* one straggler, l >= 2 */
 #define ORC_SINGLE_LT2 2 /* one straggler, 1 < l < 2: bubble filling */
 #define ORC_MULTI 3      /* m >= 2 stragglers */
+#define ORC_SERVERS 4    /* g >= 2 GPUs per server, one straggler server */
+#define ORC_MAX_SLOTS 12
 
 /* Split quantum in elements: every section and P2P chunk is a whole number
  * of quanta (the last quantum of the vector may be partial). */
@@ -75,7 +94,8 @@ typedef struct {
 } orc_step;
 
 typedef struct {
-  int p, k, m, kind, pp; /* pp = P' = number of healthy ranks */
+  int p, k, m, kind, pp; /* pp = P' = number of healthy ranks (servers when g > 1) */
+  int g, q, nseg;        /* GPUs per server, servers, segments in total */
   int64_t n;
   double ell[1024];      /* l_i = max_b / b_i */
   int ring[1024];        /* healthy ranks, ascending */
@@ -212,6 +232,22 @@ void orc_free(orc_sched *s) {
   free(s);
 }
 
+
+/* Serial order: by slot, keeping build order (segment, section, hop) within
+ * a slot (a stable counting sort). */
+static int sort_by_slot(orc_sched *s) {
+  int64_t cnt[ORC_MAX_SLOTS + 1] = {0};
+  for (int64_t i = 0; i < s->nsteps; ++i) cnt[s->steps[i].slot + 1]++;
+  for (int q = 0; q < ORC_MAX_SLOTS; ++q) cnt[q + 1] += cnt[q];
+  orc_step *sorted = (orc_step *)malloc((size_t)(s->nsteps ? s->nsteps : 1) * sizeof(orc_step));
+  if (!sorted) return -2;
+  for (int64_t i = 0; i < s->nsteps; ++i) sorted[cnt[s->steps[i].slot]++] = s->steps[i];
+  free(s->steps);
+  s->steps = sorted;
+  s->cap_steps = s->nsteps;
+  return 0;
+}
+
 /* Build the schedule for segments [seg_lo, seg_hi) (all segments when
  * seg_hi <= 0).  Returns 0, or a negative status with orc_last_error set. */
 int orc_build(int p, const double *bw, int64_t n, int k, int seg_lo, int seg_hi,
@@ -230,6 +266,9 @@ int orc_build(int p, const double *bw, int64_t n, int k, int seg_lo, int seg_hi,
   s->p = p;
   s->n = n;
   s->k = k;
+  s->g = 1;
+  s->q = p;
+  s->nseg = k;
   for (int i = 0; i < p; ++i) s->ell[i] = bmax / bw[i];
 
   /* Stragglers: ranks slower than the fastest, by l descending, then rank. */
@@ -304,26 +343,167 @@ int orc_build(int p, const double *bw, int64_t n, int k, int seg_lo, int seg_hi,
     if (dq > 0 && p2p_steps(s, g, pb, pe - pb)) { orc_free(s); g_err = "out of memory"; return -2; }
   }
 
-  /* Serial order: by slot, keeping build order (segment, section, hop)
-   * within a slot.  Counting sort over the six slots keeps it stable. */
-  int64_t cnt[7] = {0};
-  for (int64_t i = 0; i < s->nsteps; ++i) cnt[s->steps[i].slot + 1]++;
-  for (int q = 0; q < 6; ++q) cnt[q + 1] += cnt[q];
-  orc_step *sorted = (orc_step *)malloc((size_t)(s->nsteps ? s->nsteps : 1) * sizeof(orc_step));
-  if (!sorted) { orc_free(s); return -2; }
-  for (int64_t i = 0; i < s->nsteps; ++i) sorted[cnt[s->steps[i].slot]++] = s->steps[i];
-  free(s->steps);
-  s->steps = sorted;
-  s->cap_steps = s->nsteps;
+  if (sort_by_slot(s)) { orc_free(s); return -2; }
+  *out = s;
+  return 0;
+}
+
+
+/* --------------------------------------------------- several GPUs per server */
+
+/* Rank of local ring position d (0 = leader) of server sv in part i. */
+static int srank(const orc_sched *s, int sv, int part, int d) {
+  return sv * s->g + (part + d) % s->g;
+}
+
+static int chain_server(const orc_sched *s, int j, int t) {
+  int pp = s->pp;
+  return s->ring[((j + t) % pp + pp) % pp];
+}
+
+/* The steps of section j of a segment of part `part` (App. E, NVLink phases
+ * N1-N4 around Stages S1-S4).  type 1: S1-S2-S3-S4, type 2: S3-S1-S4-S2. */
+static int server_section_steps(orc_sched *s, int seg, int part, int j, int type,
+                                 int64_t off, int64_t len) {
+  int g = s->g, pp = s->pp, sv = s->strag[0], rc = 0, one[1];
+  int last = pp - 1; /* chain position of the holder */
+  /* N1: every healthy server collects its local values onto its leader. */
+  for (int h = 0; h < pp; ++h)
+    for (int d = g - 2; d >= 0; --d) {
+      one[0] = srank(s, s->ring[h], part, d + 1);
+      rc |= push_step(s, 1, seg, j, ORC_REDUCE, srank(s, s->ring[h], part, d), one, 1, off, len);
+    }
+  if (type == 2) {
+    /* N3 (type 2): the straggler server collects onto its leader ... */
+    for (int d = g - 2; d >= 0; --d) {
+      one[0] = srank(s, sv, part, d + 1);
+      rc |= push_step(s, 0, seg, j, ORC_REDUCE, srank(s, sv, part, d), one, 1, off, len);
+    }
+    /* ... S3: and sends its sum to the chain start, which adds it. */
+    one[0] = srank(s, sv, part, 0);
+    rc |= push_step(s, 2, seg, j, ORC_REDUCE, srank(s, chain_server(s, j, 0), part, 0), one, 1, off, len);
+  }
+  /* S1: reduce-scatter chain over the healthy leaders. */
+  for (int t = 1; t <= pp - 1; ++t) {
+    one[0] = srank(s, chain_server(s, j, t - 1), part, 0);
+    rc |= push_step(s, 3, seg, j, ORC_REDUCE, srank(s, chain_server(s, j, t), part, 0), one, 1, off, len);
+  }
+  int holder = srank(s, chain_server(s, j, last), part, 0);
+  if (type == 1) {
+    /* S2: the straggler leader adds the healthy partial to its own value. */
+    one[0] = holder;
+    rc |= push_step(s, 4, seg, j, ORC_REDUCE, srank(s, sv, part, 0), one, 1, off, len);
+    /* N2 (type 1): forward along the local ring, each GPU adding its own. */
+    for (int d = 1; d <= g - 1; ++d) {
+      one[0] = srank(s, sv, part, d - 1);
+      rc |= push_step(s, 5, seg, j, ORC_REDUCE, srank(s, sv, part, d), one, 1, off, len);
+    }
+    /* N3 (type 1): the global sum travels back to the leader. */
+    for (int d = g - 2; d >= 0; --d) {
+      one[0] = srank(s, sv, part, d + 1);
+      rc |= push_step(s, 6, seg, j, ORC_COPY, srank(s, sv, part, d), one, 1, off, len);
+    }
+    /* S3: straggler leader -> holder. */
+    one[0] = srank(s, sv, part, 0);
+    rc |= push_step(s, 7, seg, j, ORC_COPY, holder, one, 1, off, len);
+  }
+  /* S4: allgather over the healthy leaders from the holder. */
+  for (int t = 0; t <= pp - 2; ++t) {
+    one[0] = srank(s, chain_server(s, j, t - 1), part, 0);
+    rc |= push_step(s, 8, seg, j, ORC_COPY, srank(s, chain_server(s, j, t), part, 0), one, 1, off, len);
+  }
+  /* N4: every healthy leader distributes along its local ring. */
+  for (int h = 0; h < pp; ++h)
+    for (int d = 1; d <= g - 1; ++d) {
+      one[0] = srank(s, s->ring[h], part, d - 1);
+      rc |= push_step(s, 9, seg, j, ORC_COPY, srank(s, s->ring[h], part, d), one, 1, off, len);
+    }
+  if (type == 2) {
+    /* S2 (type 2): holder -> straggler leader; N2: distribute there. */
+    one[0] = holder;
+    rc |= push_step(s, 10, seg, j, ORC_COPY, srank(s, sv, part, 0), one, 1, off, len);
+    for (int d = 1; d <= g - 1; ++d) {
+      one[0] = srank(s, sv, part, d - 1);
+      rc |= push_step(s, 11, seg, j, ORC_COPY, srank(s, sv, part, d), one, 1, off, len);
+    }
+  }
+  return rc;
+}
+
+/* Schedule for q servers of g GPUs with one bandwidth per server, exactly
+ * one straggler server (App. E covers the single-straggler case).  k is the
+ * number of segments per part: 8 | k and k >= 24 (App. E notation). */
+int orc_build_servers(int q, int g, const double *sbw, int64_t n, int k, int seg_lo,
+                      int seg_hi, orc_sched **out) {
+  *out = NULL;
+  if (q < 3 || g < 2 || (int64_t)q * g > 1024) { g_err = "need q >= 3 servers, g >= 2, q*g <= 1024"; return -1; }
+  if (n < 0) { g_err = "N must be >= 0"; return -1; }
+  if (k < 24 || k % 8 != 0) { g_err = "n_chunks must be a multiple of 8 and >= 24"; return -1; }
+  double bmax = 0.0;
+  for (int i = 0; i < q; ++i) {
+    if (!(sbw[i] > 0.0) || !isfinite(sbw[i])) { g_err = "bandwidths must be finite and > 0"; return -1; }
+    if (sbw[i] > bmax) bmax = sbw[i];
+  }
+  orc_sched *s = (orc_sched *)calloc(1, sizeof(orc_sched));
+  if (!s) return -2;
+  s->p = q * g;
+  s->q = q;
+  s->g = g;
+  s->n = n;
+  s->k = k;
+  s->nseg = g * k;
+  s->kind = ORC_SERVERS;
+  int m = 0, pp = 0;
+  for (int sv = 0; sv < q; ++sv) {
+    if (sbw[sv] < bmax) s->strag[m++] = sv;
+    else s->ring[pp++] = sv;
+    for (int l = 0; l < g; ++l) s->ell[sv * g + l] = bmax / sbw[sv];
+  }
+  s->m = m;
+  s->pp = pp;
+  if (m != 1) { orc_free(s); g_err = "exactly one straggler server is supported"; return -3; }
+  s->seg_off = (int64_t *)calloc((size_t)s->nseg, sizeof(int64_t));
+  s->seg_len = (int64_t *)calloc((size_t)s->nseg, sizeof(int64_t));
+  s->p2p_len = (int64_t *)calloc((size_t)s->nseg, sizeof(int64_t));
+  if (!s->seg_off || !s->seg_len || !s->p2p_len) { orc_free(s); return -2; }
+  if (seg_hi <= 0 || seg_hi > s->nseg) seg_hi = s->nseg;
+  if (seg_lo < 0) seg_lo = 0;
+  s->seg_lo = seg_lo;
+  s->seg_hi = seg_hi;
+  int64_t nq = (n + ORC_QUANTUM - 1) / ORC_QUANTUM;
+  for (int part = 0; part < g; ++part) {
+    int64_t p0 = (int64_t)part * nq / g, p1 = (int64_t)(part + 1) * nq / g, lp = p1 - p0;
+    for (int sg = 0; sg < k; ++sg) {
+      int gs = part * k + sg;
+      int64_t q0 = p0 + (int64_t)sg * lp / k, q1 = p0 + (int64_t)(sg + 1) * lp / k;
+      int64_t b0 = q0 * ORC_QUANTUM < n ? q0 * ORC_QUANTUM : n;
+      int64_t e0 = q1 * ORC_QUANTUM < n ? q1 * ORC_QUANTUM : n;
+      s->seg_off[gs] = b0;
+      s->seg_len[gs] = e0 - b0;
+      if (gs < seg_lo || gs >= seg_hi) continue;
+      int type = (sg % 4 == 0 || sg % 4 == 2) ? 1 : 2;
+      int64_t rq = q1 - q0, qb = rq / pp, big = rq % pp, qcur = q0;
+      for (int j = 0; j < pp; ++j) {
+        int64_t ql = qb + (j < big ? 1 : 0);
+        int64_t b = qcur * ORC_QUANTUM, e = (qcur + ql) * ORC_QUANTUM;
+        if (b > n) b = n;
+        if (e > n) e = n;
+        if (server_section_steps(s, gs, part, j, type, b, e - b)) { orc_free(s); g_err = "out of memory"; return -2; }
+        qcur += ql;
+      }
+    }
+  }
+  if (sort_by_slot(s)) { orc_free(s); return -2; }
   *out = s;
   return 0;
 }
 
 /* ------------------------------------------------------------ accessors */
 
-int orc_info(const orc_sched *s, int64_t *out8, int *ring, int *strag, double *ell) {
-  out8[0] = s->p; out8[1] = s->k; out8[2] = s->m; out8[3] = s->kind;
-  out8[4] = s->pp; out8[5] = s->n; out8[6] = s->nsteps; out8[7] = s->nsrcpool;
+int orc_info(const orc_sched *s, int64_t *out12, int *ring, int *strag, double *ell) {
+  out12[0] = s->p; out12[1] = s->k; out12[2] = s->m; out12[3] = s->kind;
+  out12[4] = s->pp; out12[5] = s->n; out12[6] = s->nsteps; out12[7] = s->nsrcpool;
+  out12[8] = s->g; out12[9] = s->q; out12[10] = s->nseg; out12[11] = 0;
   for (int i = 0; i < s->pp; ++i) ring[i] = s->ring[i];
   for (int i = 0; i < s->m; ++i) strag[i] = s->strag[i];
   for (int i = 0; i < s->p; ++i) ell[i] = s->ell[i];
@@ -331,7 +511,7 @@ int orc_info(const orc_sched *s, int64_t *out8, int *ring, int *strag, double *e
 }
 
 void orc_segments(const orc_sched *s, int64_t *off, int64_t *len, int64_t *p2p) {
-  for (int g = 0; g < s->k; ++g) { off[g] = s->seg_off[g]; len[g] = s->seg_len[g]; p2p[g] = s->p2p_len[g]; }
+  for (int g = 0; g < s->nseg; ++g) { off[g] = s->seg_off[g]; len[g] = s->seg_len[g]; p2p[g] = s->p2p_len[g]; }
 }
 
 /* Export the steps as parallel arrays: ints[i*6 + .] = slot, seg, sec, op,

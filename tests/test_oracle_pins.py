@@ -386,3 +386,120 @@ def test_invalid_inputs(orc):
         orc.Schedule(4, [1.0, 0.0, 1.0, 1.0], 10, 4)
     with pytest.raises(orc.OracleError):
         orc.Schedule(4, [1.0, 0.5, 0.5, 0.5], 10, 4)  # one healthy rank
+
+
+# ------------------------------------------- several GPUs per server (App. E)
+SERVER_CASES = [(3, 2, {1: 0.5}), (4, 2, {3: 0.75}), (4, 3, {0: 0.5}), (5, 4, {2: 0.25}),
+                (3, 4, {2: 0.875}), (6, 2, {5: 0.5})]
+
+
+def _sbw(q, slow):
+    return _bw(q, slow)
+
+
+@pytest.mark.parametrize("q,g,slow", SERVER_CASES)
+@pytest.mark.parametrize("n", [0, 1, 63, 64 * 3 * 24 + 5, 5000])
+def test_servers_int32_exact_and_provenance(orc, q, g, slow, n):
+    """App. E schedule, Sec. 3 correctness: exact int32 sums on every rank and
+    no rank counted twice."""
+    s = orc.Schedule.servers(q, g, _sbw(q, slow), n, 24)
+    assert s.kind == "servers" and s.p == q * g
+    x = _rand("i32", s.p, n, 3 * q + g + n)
+    y = orc.run(s, "i32", x.copy())
+    assert (y == orc.brute_sum("i32", x)[None, :]).all()
+    if 0 < n <= 300:
+        ok, msg = orc.provenance(s)
+        assert ok, msg
+
+
+@pytest.mark.parametrize("q,g,slow", SERVER_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_servers_float_error_bound(orc, q, g, slow, dtype):
+    n = 64 * 40 + 3
+    s = orc.Schedule.servers(q, g, _sbw(q, slow), n, 24)
+    x = _rand(dtype, s.p, n, 5 * q + g)
+    y = orc.run(s, dtype, x.copy())
+    assert (y == y[0][None, :]).all()
+    got = y[0].astype(np.float64) if dtype == "f32" else orc.bf16_to_f64(y[0])
+    assert (np.abs(got - orc.brute_sum(dtype, x)) <= orc.tolerance(dtype, s.p, x)).all()
+
+
+@pytest.mark.parametrize("q,g,slow", SERVER_CASES)
+def test_servers_nic_volumes(orc, q, g, slow):
+    """App. B.3 lemmas: every coordinate crosses server boundaries at least
+    2(q-1) times, and the slow server sends and receives every coordinate;
+    this schedule meets both exactly (2(q-1)N inter-server elements, N out of
+    and N into the slow server)."""
+    n = 64 * 2 * 24 * 3 + 7
+    s = orc.Schedule.servers(q, g, _sbw(q, slow), n, 24)
+    sv = int(s.stragglers[0])
+    inter = sent = recv = 0
+    for (_, src, dst, _, ln, _) in s.flows():
+        if src // g != dst // g:
+            inter += ln
+            sent += ln if src // g == sv else 0
+            recv += ln if dst // g == sv else 0
+    assert inter == 2 * (q - 1) * n
+    assert sent == n and recv == n
+
+
+@pytest.mark.parametrize("q,g,slow", [(4, 3, {0: 0.5}), (5, 2, {4: 0.75})])
+def test_servers_stage_semantics(orc, q, g, slow):
+    """App. E: after N1 every healthy leader holds its server's local sum;
+    in type 1 the end of the straggler's ring holds the global sum after N2;
+    in type 2 the holder's leader holds it after S1."""
+    n, k = 64 * (q - 1) * 24 * g, 24
+    s = orc.Schedule.servers(q, g, _sbw(q, slow), n, k)
+    sv = int(s.stragglers[0])
+    full = (1 << s.p) - 1
+    after = {h: _sets_after(s, h, n) for h in (2, 4, 6)}
+    for seg in range(s.nseg):
+        part, sg = divmod(seg, k)
+        c = int(s.seg_off[seg])
+        if s.seg_len[seg] == 0:
+            continue
+        for h in s.ring:
+            leader = int(h) * g + part
+            assert after[2][leader][c] == sum(1 << (int(h) * g + l) for l in range(g))
+        typ = 1 if sg % 4 in (0, 2) else 2
+        if typ == 1:
+            end = sv * g + (part + g - 1) % g
+            assert after[6][end][c] == full
+        else:
+            # section 0 of the segment: chain starts at ring[0], holder ring[-1]
+            holder = int(s.ring[-1]) * g + part
+            assert after[4][holder][c] == full
+
+
+def test_servers_bounds_and_model():
+    """Theorem 3 (Sec. 3 form max{2l(p-g)/(g(l(p-g)+g)), l/g} n) equals its
+    App. B.3 form; g = 1 recovers Theorem 1 and the tight single bound; the
+    App. E time stays within q/(q-1) of the tight bound for l < 2 as k grows
+    and above it always."""
+    for q, g in [(4, 2), (8, 8), (16, 4), (33, 3)]:
+        p = q * g
+        for ell in [F(9, 8), F(3, 2), F(2), F(3)]:
+            sec3 = max(2 * ell * (p - g) / (g * (ell * (p - g) + g)), ell / g)
+            assert sec3 == model.lb_servers_weak(q, g, ell, 1)
+            assert model.lb_servers_tight(q, g, ell, 1) >= model.lb_servers_weak(q, g, ell, 1)
+            t = model.optcc_servers(q, g, ell, 1, 10**9)
+            assert t >= model.lb_servers_tight(q, g, ell, 1)
+            if ell < 2:
+                assert t / model.lb_servers_tight(q, g, ell, 1) < F(q, q - 1) * (1 + F(1, 10**6))
+            for k in (24, 64):
+                assert model.optcc_servers(q, g, ell, 1, k) >= model.lb_servers_tight(q, g, ell, 1)
+    for p in [5, 9]:
+        for ell in [F(3, 2), F(5, 2)]:
+            assert model.lb_servers_weak(p, 1, ell, 7) == model.lb_weak_single(p, ell, 7)
+            assert model.lb_servers_tight(p, 1, ell, 7) == model.lb_tight_single(p, ell, 7)
+
+
+def test_servers_invalid(orc):
+    with pytest.raises(orc.OracleError):
+        orc.Schedule.servers(4, 2, [1, 1, 1, 1], 100, 24)  # no straggler server
+    with pytest.raises(orc.OracleError):
+        orc.Schedule.servers(4, 2, [1, 0.5, 0.5, 1], 100, 24)  # two
+    with pytest.raises(orc.OracleError):
+        orc.Schedule.servers(4, 2, [1, 0.5, 1, 1], 100, 20)  # 8 does not divide k
+    with pytest.raises(orc.OracleError):
+        orc.Schedule.servers(4, 2, [1, 0.5, 1, 1], 100, 16)  # k < 24
