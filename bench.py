@@ -45,11 +45,14 @@ def measured_traffic(workload: str, launches: int):
 
 def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
     """The oracle, untuned, on a bounded sample of whole segments (serial, one
-    host thread), reported in the metric's unit."""
+    host thread), reported in the metric's unit.  When the whole workload
+    runs in less than the budget it is run again (inputs restored, untimed)
+    until the budget is spent, and the mean is reported."""
     import numpy as np
     import oracle
 
     off, ln, _ = plan.segments()
+    total = plan.num_segments
     host = None
 
     def run(nseg):
@@ -63,19 +66,26 @@ def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
             host[:, :end] = src.view(torch.int16).numpy().view(np.uint16)
         else:
             host[:, :end] = src.numpy()
-        sched = oracle.Schedule(w.p, w.bandwidths, w.n, w.k, seg_lo=0, seg_hi=nseg)
+        if w.g > 1:
+            sched = oracle.Schedule.servers(w.q, w.g, w.bandwidths, w.n, w.k, seg_lo=0, seg_hi=nseg)
+        else:
+            sched = oracle.Schedule(w.p, w.bandwidths, w.n, w.k, seg_lo=0, seg_hi=nseg)
         t = time.perf_counter()
         oracle.run(sched, w.dtype, host)
         return time.perf_counter() - t, end
 
     t1, _ = run(1)
-    nseg = int(max(1, min(w.k, budget_s / max(t1, 1e-6))))
-    t, elems = run(nseg)
+    nseg = int(max(1, min(total, budget_s / max(t1, 1e-6))))
+    times = []
+    while not times or (nseg == total and sum(times) < budget_s and len(times) < 20):
+        t, elems = run(nseg)
+        times.append(t)
+    t = sum(times) / len(times)
     bytes_sample = traffic_bytes * elems / w.n
     return {"value": round(bytes_sample / t / 1e9, 4), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"first {nseg} of {w.k} segments ({elems} of {w.n} elements per rank), "
-                      f"serial C oracle, {t:.2f} s"}
+            "sample": f"first {nseg} of {total} segments ({elems} of {w.n} elements per rank), "
+                      f"serial C oracle, mean of {len(times)} run(s) of {t:.2f} s"}
 
 
 def copy_bench(torch, args):
@@ -131,13 +141,16 @@ def main():
     w = WORKLOADS[args.workload]
     x = make_inputs(w, device="cuda:0")
     x0 = x.clone()
-    plan = optcc.optcc_plan(w.p, w.bandwidths, w.n, w.k)
-    rd, wr = plan.traffic(w.dtype, 0, optcc.OPTCC_NUM_SLOTS, args.launches)
+    if w.g > 1:  # q servers of g GPUs (App. E)
+        plan = optcc.optcc_plan_servers(w.q, w.g, w.bandwidths, w.n, w.k)
+    else:
+        plan = optcc.optcc_plan(w.p, w.bandwidths, w.n, w.k)
+    nslots = plan.num_slots
+    rd, wr = plan.traffic(w.dtype, 0, nslots, args.launches)
     alg_bytes = rd + wr
 
     def step():
-        optcc.optcc_allreduce_emulate_slots(x, w.p, w.n, w.dtype, plan, 0,
-                                            optcc.OPTCC_NUM_SLOTS, args.launches)
+        optcc.optcc_allreduce_emulate_slots(x, w.p, w.n, w.dtype, plan, 0, nslots, args.launches)
 
     for _ in range(args.warmup):
         step()
@@ -184,8 +197,11 @@ def main():
     traffic = measured_traffic(w.name, args.launches)
     n = w.n
     t_model = optcc.optcc_model_time(plan) / n
-    lb = optcc.optcc_lower_bound(w.p, w.bandwidths, n) / n
-    t0_ring = 2.0 * (w.p - 1) / w.p
+    if w.g > 1:
+        lb = optcc.optcc_lower_bound_servers(w.q, w.g, w.bandwidths, n) / n
+    else:
+        lb = optcc.optcc_lower_bound(w.p, w.bandwidths, n) / n
+    t0_ring = 2.0 * (w.p - 1) / (w.g * w.p)  # fault-free optimum with g GPUs per server
     # the same flows timed in the paper's network model (list scheduling)
     evaluated = None
     if plan.num_flows <= (1 << 20):
@@ -205,8 +221,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": w.name, "p": w.p, "N": w.n, "n_chunks": w.k,
+            "gpus_per_server": w.g,
             "stragglers": {str(int(r)): float(w.bandwidths[int(r)]) for r in plan.stragglers},
-            "values": w.values, "launches_per_step": 1 if args.launches == 1 else 6,
+            "values": w.values, "launches_per_step": 1 if args.launches == 1 else nslots,
             "plan_kind": plan.kind,
         },
         "roofline": {

@@ -39,7 +39,9 @@ extern "C" {
 
 #define OPTCC_MAX_RANKS 1024        /* largest p a plan accepts */
 #define OPTCC_MAX_EMULATE_RANKS 256 /* largest p the GPU executor accepts */
-#define OPTCC_NUM_SLOTS 6           /* stage slots, see optcc_allreduce_emulate_slots */
+#define OPTCC_NUM_SLOTS 6           /* stage slots of a one-GPU-per-server plan */
+#define OPTCC_NUM_SERVER_SLOTS 12   /* stage slots of a several-GPUs-per-server plan */
+#define OPTCC_MAX_GPUS_PER_SERVER 64 /* largest g optcc_plan_servers accepts */
 #define OPTCC_QUANTUM 64            /* split quantum in elements */
 
 typedef struct optcc_plan optcc_plan_t;
@@ -50,7 +52,8 @@ typedef enum {
   OPTCC_KIND_RING = 0,       /* no straggler: the ring of Sec. 3 (T0) */
   OPTCC_KIND_SINGLE_GE2 = 1, /* one straggler with l >= 2 (Sec. 4.3, first case) */
   OPTCC_KIND_SINGLE_LT2 = 2, /* one straggler with l < 2: bubble filling (Sec. 4.2, App. C) */
-  OPTCC_KIND_MULTI = 3       /* m >= 2 stragglers (App. D) */
+  OPTCC_KIND_MULTI = 3,      /* m >= 2 stragglers (App. D) */
+  OPTCC_KIND_SERVERS = 4     /* g >= 2 GPUs per server, one straggler server (App. E) */
 } optcc_kind_t;
 
 /*
@@ -76,6 +79,40 @@ typedef enum {
  */
 int optcc_plan(int p, const double *link_bandwidths, int64_t N, int n_chunks,
                optcc_plan_t **out);
+
+/*
+ * optcc_plan_servers - build the OptCC schedule for q servers of g GPUs each
+ * with one straggler server (App. E: NVLink phases N1-N4 around the four NIC
+ * stages, two schedule types, no bubble filling).
+ *
+ *   q, g              servers and GPUs per server: q >= 3, 2 <= g <=
+ *                     OPTCC_MAX_GPUS_PER_SERVER, p = q*g <= OPTCC_MAX_RANKS.
+ *                     Ranks are numbered server-major: rank = server*g + local
+ *                     index.
+ *   server_bandwidths host array of q finite values > 0: one NIC bandwidth per
+ *                     server (PXN pools a server's NICs, Sec. 2, so all its
+ *                     GPUs share one slowdown l = max(b)/b).  Exactly one
+ *                     server must be slower than the fastest.
+ *   N                 elements per rank, N >= 0
+ *   n_chunks          k, segments per part: a multiple of 8 and >= 24 (App. E
+ *                     notation: the pattern overlay needs 8 | k and k >= 24)
+ *   out               receives the plan; untouched on failure
+ *
+ * Split: the vector's NQ = ceil(N/64) quanta form g parts, part i =
+ * [floor(i*NQ/g), floor((i+1)*NQ/g)), led by local GPU i of every server;
+ * each part is cut into k segments like optcc_plan (segment index part*k + c),
+ * and each segment into q-1 sections (one per healthy server), the first
+ * (rem) one quantum larger.  Segment c of a part uses schedule type 1
+ * (S1-S2-S3-S4, patterns A and C) when c mod 4 is 0 or 2, type 2
+ * (S3-S1-S4-S2, patterns B and D) otherwise.  Local ring of part i on every
+ * server: position d is local GPU (i + d) mod g; collect phases run it
+ * backwards onto the leader (d = 0), distribute phases forwards.
+ * The plan's ring[] and stragglers[] hold server indices.
+ * Errors: OPTCC_EINVAL (bad q/g/N/k/bandwidths), OPTCC_EUNSUPPORTED (no or
+ * several straggler servers, p over the limit), OPTCC_ENOMEM.  No device call.
+ */
+int optcc_plan_servers(int q, int g, const double *server_bandwidths, int64_t N, int n_chunks,
+                       optcc_plan_t **out);
 
 /* Free a plan and its device tables.  The caller guarantees that no emulation
  * using it is still running on any stream.  NULL is ignored. */
@@ -110,14 +147,30 @@ int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t d
  * optcc_allreduce_emulate_slots - execute only the steps whose stage slot is
  * in [slot_begin, slot_end), either fused in one launch (launches = 1) or as
  * one launch per slot (launches = 0), same buffers and errors as above.
- * Slots (each section uses a subset, always in increasing order):
+ * Slots of a one-GPU-per-server plan (each section uses a subset, always in
+ * increasing order):
  *   0  stragglers' raw values folded into the chain start (ordering 2, Sec. 4.1;
  *      the non-finalising stragglers of A'/C', App. D)
  *   1  Stage 1 reduce-scatter chain        2  Stage 2 upload; P2P up (App. C)
  *   3  Stage 3 download; P2P down          4  Stage 4 allgather
  *   5  global sum to the stragglers that did not finalise (ordering 2 Stage 2)
+ * Slots of a several-GPUs-per-server plan (App. E; "leader" = local ring
+ * position 0 of the section's part, type = schedule type of the segment):
+ *   0  N3 collect onto the straggler server's leader (type 2)
+ *   1  N1 collect onto every healthy server's leader
+ *   2  S3: the straggler leader's sum added into the chain start (type 2)
+ *   3  S1 reduce-scatter chain over the healthy leaders
+ *   4  S2: the straggler leader adds the holder's partial (type 1)
+ *   5  N2 fold: forward along the straggler's local ring, each GPU adding
+ *      its own value (type 1)
+ *   6  N3: the global sum copied back along the straggler's ring (type 1)
+ *   7  S3: straggler leader -> holder (type 1)
+ *   8  S4 allgather over the healthy leaders
+ *   9  N4 distribute on every healthy server
+ *   10 S2: holder -> straggler leader (type 2)
+ *   11 N2 distribute on the straggler server (type 2)
  * After [0, s) the buffers equal the state after the first s slots of every
- * section; [0, 6) is the whole AllReduce.
+ * section; [0, 6) (or [0, 12)) is the whole AllReduce.
  */
 int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
                                   const optcc_plan_t *plan, int slot_begin, int slot_end,
@@ -131,9 +184,11 @@ int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N, optcc_dty
  *   one, l >= 2       l N (k+1)/k                                   (Sec. 4.3)
  *   one, l < 2        2(p-1) l N/((p-2)l+2) * (k+l-1)/k             (Sec. 4.3, App. C)
  *   m >= 2            (k+4) max{2(p-1)s, (l_1(p-m)+2(m-1))s}, s = N/(k(p-m))  (App. D)
+ *   g GPUs/server     max{l, 2} N (k+5.5)/(g k)                     (App. E time analysis)
  * link_bandwidths may be NULL (use the plan's) or must give the same
- * stragglers and slowdowns (relative difference <= 1e-12).  Returns NaN on
- * error, with optcc_last_error set.
+ * stragglers and slowdowns (relative difference <= 1e-12): p entries, or q
+ * (one per server) for a server plan.  Returns NaN on error, with
+ * optcc_last_error set.
  */
 double optcc_model_time(const optcc_plan_t *plan, const double *link_bandwidths);
 
@@ -146,6 +201,16 @@ double optcc_model_time(const optcc_plan_t *plan, const double *link_bandwidths)
  */
 double optcc_lower_bound(int p, const double *link_bandwidths, int64_t N);
 
+/*
+ * optcc_lower_bound_servers - best known lower bound for q servers of g GPUs
+ * with one straggler server, same unit (tight multi-GPU bound, App. B.3):
+ *   (N/g) max{2l(q-1)/(l(q-2)+2), l};  without a straggler the fault-free
+ *   optimum 2(p-1)N/(g p) with p = q g (Sec. 3).
+ * Returns NaN on invalid input (q < 3, g < 1, bad bandwidths, N < 0, or more
+ * than one straggler server).
+ */
+double optcc_lower_bound_servers(int q, int g, const double *server_bandwidths, int64_t N);
+
 /* Message of the last failure on the calling thread ("" if none). */
 const char *optcc_last_error(void);
 
@@ -154,26 +219,30 @@ const char *optcc_last_error(void);
 
 typedef struct {
   int32_t p, k, m, kind;
-  int32_t healthy;  /* P' = p - m */
+  int32_t healthy;  /* P' = p - m (healthy servers q - 1 for a server plan) */
   int32_t quantum;  /* OPTCC_QUANTUM */
   int64_t n;
   int64_t num_steps; /* steps: one destination write each */
   int64_t num_flows; /* flows: one per (step, source rank) */
+  int32_t g, q;          /* GPUs per server (1 for optcc_plan) and servers */
+  int32_t num_segments;  /* k, or g*k for a server plan */
+  int32_t num_slots;     /* OPTCC_NUM_SLOTS or OPTCC_NUM_SERVER_SLOTS */
 } optcc_plan_info_t;
 
-/* Fill info and, when non-NULL, ring[P'] (healthy ranks in ring order),
- * stragglers[m] (sorted) and slowdowns[p]. */
+/* Fill info and, when non-NULL, ring[P'] (healthy ranks in ring order; server
+ * indices for a server plan), stragglers[m] (sorted; servers likewise) and
+ * slowdowns[p] (per rank). */
 int optcc_plan_info(const optcc_plan_t *plan, optcc_plan_info_t *info, int32_t *ring,
                     int32_t *stragglers, double *slowdowns);
 
-/* Per segment (k entries each): element offset, length, and length of the
- * trailing point-to-point chunk (0 unless bubble filling). */
+/* Per segment (num_segments entries each): element offset, length, and
+ * length of the trailing point-to-point chunk (0 unless bubble filling). */
 int optcc_plan_segments(const optcc_plan_t *plan, int64_t *offset, int64_t *length,
                         int64_t *p2p_length);
 
 typedef struct {
-  int32_t slot;    /* 0..5, see optcc_allreduce_emulate_slots */
-  int32_t segment; /* 0..k-1 */
+  int32_t slot;    /* 0..num_slots-1, see optcc_allreduce_emulate_slots */
+  int32_t segment; /* 0..num_segments-1 */
   int32_t section; /* 0..P'-1, or -1 for the point-to-point chunk */
   int32_t op;      /* 0 copy, 1 reduce (dst += src) */
   int32_t src, dst;

@@ -16,23 +16,28 @@ namespace {
 
 using namespace kern;
 
-template <class D>
+template <class D, bool S>
 hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   constexpr int W16 = 16 / (int)sizeof(typename D::S);
   const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
   if (!vec16) {
-    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S>), grid, block, 0, st, a);
     return hipGetLastError();
   }
   if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
     if (two) {
-      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S>), grid, block, 0, st, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1>), grid, block, 0, st, a);
+  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S>), grid, block, 0, st, a);
   return hipGetLastError();
+}
+
+template <class D>
+hipError_t launch_plan(const KArgs &a, bool servers, bool vec16, bool two, hipStream_t st) {
+  return servers ? launch<D, true>(a, vec16, two, st) : launch<D, false>(a, vec16, two, st);
 }
 
 int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
@@ -47,7 +52,7 @@ int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
   }
   // Tiles: 2048-element pieces of every segment's ring part and P2P chunk.
   std::vector<TileDesc> tiles;
-  for (int g = 0; g < pl.k; ++g) {
+  for (int g = 0; g < pl.nseg; ++g) {
     const Segment &s = pl.seg[(size_t)g];
     auto cut = [&](int64_t b, int64_t e, int is_p2p) {
       for (int64_t x = b; x < e; x += kTileElems) {
@@ -88,7 +93,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   if (p != pl->p || N != pl->n) return fail(OPTCC_EINVAL, "p or N differ from the plan's");
   if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
     return fail(OPTCC_EINVAL, "unknown dtype");
-  if (sb < 0 || se > OPTCC_NUM_SLOTS || sb > se) return fail(OPTCC_EINVAL, "slot range must satisfy 0 <= begin <= end <= 6");
+  if (sb < 0 || se > pl->nslots || sb > se)
+    return fail(OPTCC_EINVAL, "slot range must satisfy 0 <= begin <= end <= " + std::to_string(pl->nslots));
   if (launches != 0 && launches != 1) return fail(OPTCC_EINVAL, "launches must be 0 (one per slot) or 1 (fused)");
   if (p > kMaxRanks) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_EMULATE_RANKS");
   if (N == 0 || sb == se) return OPTCC_OK;  // nothing to move; pointers are not touched
@@ -119,22 +125,33 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   a.n = N;
   a.pp = pl->pp;
   a.m = pl->m;
-  for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
-  for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
+  a.g = pl->g;
+  const bool servers = pl->kind == OPTCC_KIND_SERVERS;
+  if (servers) {  // per server (healthy in ring order, then the straggler): its g GPUs
+    const int g = pl->g;
+    for (int h = 0; h < pl->pp; ++h)
+      for (int l = 0; l < g; ++l) a.ptr[h * g + l] = bufs[pl->ring[(size_t)h] * g + l];
+    for (int l = 0; l < g; ++l) a.ptr[pl->pp * g + l] = bufs[pl->strag[0] * g + l];
+  } else {
+    for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
+    for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
-  // short chains: two vectors per lane and per-XCD tile runs (both measured
-  // faster up to 32 healthy ranks and neutral or slower beyond)
-  const bool two = pl->pp <= kTwoVectorMaxHealthy;
-  a.xcd_runs = pl->pp <= kTwoVectorMaxHealthy ? 1 : 0;
+  // short chains (inputs per lane: P' for one GPU per server, p for several):
+  // two vectors per lane and per-XCD tile runs (both measured faster up to
+  // 32 and neutral or slower beyond)
+  const int chain = servers ? pl->p : pl->pp;
+  const bool two = chain <= kTwoVectorMaxHealthy;
+  a.xcd_runs = chain <= kTwoVectorMaxHealthy ? 1 : 0;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
     a.se = launches == 1 ? se : sb + l + 1;
     hipError_t err = hipSuccess;
     switch (dtype) {
-      case OPTCC_F32: err = launch<F32>(a, vec16, two, st); break;
-      case OPTCC_BF16: err = launch<BF16>(a, vec16, false, st); break;
-      default: err = launch<I32>(a, vec16, two, st); break;
+      case OPTCC_F32: err = launch_plan<F32>(a, servers, vec16, two, st); break;
+      case OPTCC_BF16: err = launch_plan<BF16>(a, servers, vec16, false, st); break;
+      default: err = launch_plan<I32>(a, servers, vec16, two, st); break;
     }
     if (err != hipSuccess)
       return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));
@@ -149,7 +166,7 @@ using namespace optcc;
 
 extern "C" int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
                                        const optcc_plan_t *plan, void *stream) {
-  return emulate(bufs, p, N, dtype, plan, 0, OPTCC_NUM_SLOTS, 1, stream);
+  return emulate(bufs, p, N, dtype, plan, 0, plan ? plan->nslots : OPTCC_NUM_SLOTS, 1, stream);
 }
 
 extern "C" int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N,

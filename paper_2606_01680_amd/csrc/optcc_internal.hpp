@@ -20,8 +20,8 @@ struct SegDesc {
   int64_t p2p_begin;
   int32_t qbase;
   int32_t nbig;
-  int32_t ordering;  // 1: S1-S2-S3-S4, 2: S3-S1-S4-S2 (Sec. 4.1)
-  int32_t pad;
+  int32_t ordering;  // 1: S1-S2-S3-S4, 2: S3-S1-S4-S2 (Sec. 4.1; App. E types 1, 2)
+  int32_t part;      // several GPUs per server: the part (leading local GPU), else 0
 };
 static_assert(sizeof(SegDesc) == 32, "SegDesc layout");
 
@@ -54,16 +54,19 @@ struct Segment {
   int64_t p2p_begin = 0, p2p_end = 0;   // point-to-point chunk (may be empty)
   int64_t qbase = 0, nbig = 0;
   int ordering = 1;
+  int part = 0;  // several GPUs per server: part index (App. E)
 };
 
 }  // namespace optcc
 
 struct optcc_plan {
   int p = 0, k = 0, m = 0, kind = 0, pp = 0;
+  int g = 1, q = 0;           // GPUs per server and servers (g = 1, q = p for optcc_plan)
+  int nseg = 0, nslots = 0;   // segments in total (k or g*k) and stage slots
   int64_t n = 0;
   std::vector<double> ell;    // slowdown per rank
-  std::vector<int> ring;      // healthy ranks, ascending
-  std::vector<int> strag;     // stragglers, l descending, ties lower rank
+  std::vector<int> ring;      // healthy ranks (servers when g > 1), ascending
+  std::vector<int> strag;     // stragglers (servers when g > 1), l descending, ties lower
   std::vector<optcc::Segment> seg;
   std::vector<optcc::SegDesc> segdesc;
   std::vector<optcc::TileDesc> tiles;

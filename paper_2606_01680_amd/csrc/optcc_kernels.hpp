@@ -62,8 +62,11 @@ struct KArgs {
   int32_t pp, m;
   int32_t sb, se;  // slot range [sb, se)
   int32_t xcd_runs;  // 1: each XCD takes a contiguous run of tiles
-  // rank pointers: [0, pp) healthy ranks in ring order, [pp, pp+m) stragglers
-  // sorted by slowdown (worst first)
+  int32_t g;         // GPUs per server (1: one rank per server)
+  // rank pointers.  g = 1: [0, pp) healthy ranks in ring order, [pp, pp+m)
+  // stragglers sorted by slowdown (worst first).  g > 1: [h*g, h*g+g) the g
+  // GPUs (by local index) of the h-th healthy server in ring order, then the
+  // straggler server's g GPUs at [pp*g, pp*g+g).
   void *ptr[kMaxRanks];
 };
 
@@ -341,6 +344,228 @@ __device__ void p2p_lane(const KArgs &a, void *const *rp, const int64_t (&e)[L])
   }
 }
 
+// ------------------------------------------ several GPUs per server (App. E)
+// Every step of one section of a part for L vectors per lane.  Each server's
+// g GPUs form a local ring; position d of the part's ring is local GPU
+// (part + d) mod g, position 0 the part's leader.  Collect phases (N1, N3 of
+// type 2) run the ring backwards onto the leader, each GPU adding its own
+// value; distribute phases (N2 of type 2, N4) copy forwards.  The NIC stages
+// S1-S4 run among the leaders as in the one-GPU case.
+//   type 1 (S1-S2-S3-S4): N1, S1, S2 (the straggler leader adds the holder's
+//     partial), N2 fold (forward along the straggler's ring, each GPU adding
+//     its own value: the last one holds the global sum), N3 (the sum copied
+//     back to the leader), S3 (to the holder), S4, N4
+//   type 2 (S3-S1-S4-S2): N3 collect on the straggler, N1, S3 (the
+//     straggler's sum added into the chain start), S1, S4, N4, S2 (global sum
+//     to the straggler leader), N2 distribute
+// Every input value is read once, in the order the steps consume it: that
+// flat sequence (straggler collect, then each chain server's collect, then
+// the straggler's fold operands) is prefetched through a rolling window of B
+// loads.  Partial sums stay in registers; every step writes its destination.
+__device__ __forceinline__ int local_gpu(int part, int d, int g) {
+  const int i = part + d;
+  return i >= g ? i - g : i;
+}
+
+template <class D, int W, int L, int B>
+__device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, const SegDesc &sd, const int (&j)[L],
+                            const int64_t (&e)[L]) {
+  using V = Vec<D, W>;
+  const int pp = a.pp, g = a.g, part = sd.part;
+  const bool t1 = sd.ordering == 1;
+  // buffer of chain position t (server R[j+t], 0 <= t < pp) at local position d
+  auto hr = [&](int l, int t, int d) __attribute__((always_inline)) {
+    int h = j[l] + t;
+    h = h >= pp ? h - pp : h;
+    return rp[h * g + local_gpu(part, d, g)];
+  };
+  auto sr = [&](int d) __attribute__((always_inline)) { return rp[pp * g + local_gpu(part, d, g)]; };
+  const bool i0 = !t1 && in_range(a, 0), i1 = in_range(a, 1), i2 = !t1 && in_range(a, 2);
+  const bool i3 = in_range(a, 3), i4 = t1 && in_range(a, 4), i5 = t1 && in_range(a, 5);
+  V v[L], acc[L], ss[L];
+  bool have = false;  // v holds the value the next step reads
+
+  // Slots 2/3 without slot 1 (partial slot ranges only): the leaders already
+  // hold their collected values.
+  if (!i1 && (i2 || i3)) {
+#pragma unroll
+    for (int l = 0; l < L; ++l) v[l] = ld_in<D, W>(hr(l, 0, 0), e[l]);
+    if (i2) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        v[l] = add2<D, W>(ld_in<D, W>(sr(0), e[l]), v[l]);
+        st_mid<D, W>(hr(l, 0, 0), e[l], v[l]);
+      }
+    }
+    if (i3)
+      for (int t = 1; t < pp; ++t) {
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          v[l] = add2<D, W>(ld_in<D, W>(hr(l, t, 0), e[l]), v[l]);
+          st_mid<D, W>(hr(l, t, 0), e[l], v[l]);
+        }
+      }
+    have = i3;
+  }
+
+  // The flat input sequence: [0, nA) straggler collect (slot 0), [nA, nA+nB)
+  // chain servers' collects (slot 1, with slots 2/3 folded in at each
+  // leader), then the straggler's operands of slots 4/5.
+  const int nA = i0 ? g : 0, nB = i1 ? pp * g : 0;
+  const int n = nA + nB + (i4 ? 1 : 0) + (i5 ? g - 1 : 0);
+  const int c0 = i4 ? 0 : 1;  // straggler position of the first slot-4/5 operand
+  struct Cur {
+    int i, t, d;  // flat index; chain position and local position inside [nA, nA+nB)
+  };
+  auto cur_ptr = [&](int l, const Cur &c) __attribute__((always_inline)) {
+    if (c.i < nA) return sr(g - 1 - c.i);
+    if (c.i < nA + nB) return hr(l, c.t, c.d);
+    return sr(c.i - nA - nB + c0);
+  };
+  auto cur_next = [&](Cur &c) __attribute__((always_inline)) {
+    if (c.i >= nA && c.i < nA + nB && --c.d < 0) {
+      c.d = g - 1;
+      ++c.t;
+    }
+    ++c.i;
+  };
+  // Every input value feeds one running sum `acc`: the collects (slots 0, 1)
+  // start from the raw value at the far end of a local ring and add one GPU
+  // per step; the straggler's S2 and N2 fold (slots 4, 5) continue from the
+  // holder's partial.  The chain steps (slots 2, 3) run when a leader's
+  // collect completes.
+  auto consume = [&](const Cur &c, const V (&x)[L]) __attribute__((always_inline)) {
+    const bool inA = c.i < nA, inB = !inA && c.i < nA + nB, inC = !inA && !inB;
+    const int d = inA ? g - 1 - c.i : (inB ? c.d : c.i - nA - nB + c0);
+    const bool raw = !inC && d == g - 1;  // the far end of a collect: no step
+    if (inC && c.i == nA + nB) {           // first of slots 4/5: the state it continues
+#pragma unroll
+      for (int l = 0; l < L; ++l) acc[l] = have ? v[l] : ld_in<D, W>(d == 0 ? hr(l, pp - 1, 0) : sr(0), e[l]);
+    }
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      acc[l] = raw ? x[l] : add2<D, W>(x[l], acc[l]);
+      if (!raw) {
+        void *dst = inB ? hr(l, c.t, d) : sr(d);
+        if (inC && d == g - 1) st_fin<D, W>(dst, e[l], acc[l]);  // the global sum
+        else st_mid<D, W>(dst, e[l], acc[l]);
+      }
+    }
+    if (inA && d == 0) {  // the straggler leader holds its server's sum
+#pragma unroll
+      for (int l = 0; l < L; ++l) ss[l] = acc[l];
+    }
+    if (inB && d == 0) {  // leader t holds its server's sum
+      if (c.t == 0) {
+        if (i2) {  // slot 2: S3 into the chain start (type 2)
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            const V s2 = i0 ? ss[l] : ld_in<D, W>(sr(0), e[l]);
+            v[l] = add2<D, W>(s2, acc[l]);
+            st_mid<D, W>(hr(l, 0, 0), e[l], v[l]);
+          }
+        } else {
+#pragma unroll
+          for (int l = 0; l < L; ++l) v[l] = acc[l];
+        }
+      } else if (i3) {  // slot 3: S1 hop into leader t
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          v[l] = add2<D, W>(acc[l], v[l]);
+          st_mid<D, W>(hr(l, c.t, 0), e[l], v[l]);
+        }
+      }
+      if (c.t == pp - 1) have = i3;
+    }
+  };
+  {
+    V buf[B][L];
+    Cur pc{0, 0, g - 1}, cc{0, 0, g - 1};
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+      if (u < n) {
+#pragma unroll
+        for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W>(cur_ptr(l, pc), e[l]);
+        cur_next(pc);
+      }
+    for (int t0 = 0; t0 < n; t0 += B) {
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (t0 + u < n) {
+          consume(cc, buf[u]);
+          cur_next(cc);
+          if (t0 + u + B < n) {
+#pragma unroll
+            for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W>(cur_ptr(l, pc), e[l]);
+            cur_next(pc);
+          }
+        }
+    }
+  }
+  if (i4 || i5) {  // slots 4/5 ran: the straggler's running sum is the state
+#pragma unroll
+    for (int l = 0; l < L; ++l) v[l] = acc[l];
+    have = true;
+  }
+
+  if (t1 && in_range(a, 6)) {  // slot 6: N3, the global sum back to the leader
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+      if (!have) v[l] = ld_in<D, W>(sr(g - 1), e[l]);
+    for (int d = g - 2; d >= 0; --d) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(sr(d), e[l], v[l]);
+    }
+    have = true;
+  }
+  if (t1 && in_range(a, 7)) {  // slot 7: S3, straggler leader -> holder
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      if (!have) v[l] = ld_in<D, W>(sr(0), e[l]);
+      st_fin<D, W>(hr(l, pp - 1, 0), e[l], v[l]);
+    }
+    have = true;
+  }
+  if (in_range(a, 8)) {  // slot 8: S4 allgather from the holder
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+      if (!have) v[l] = ld_in<D, W>(hr(l, pp - 1, 0), e[l]);
+    for (int t = 0; t + 1 < pp; ++t) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(hr(l, t, 0), e[l], v[l]);
+    }
+    have = true;
+  }
+  if (in_range(a, 9)) {  // slot 9: N4 distribute on every healthy server
+    for (int t = 0; t < pp; ++t) {
+      V gt[L];
+#pragma unroll
+      for (int l = 0; l < L; ++l) gt[l] = have ? v[l] : ld_in<D, W>(hr(l, t, 0), e[l]);
+      for (int d = 1; d < g; ++d) {
+#pragma unroll
+        for (int l = 0; l < L; ++l) st_fin<D, W>(hr(l, t, d), e[l], gt[l]);
+      }
+    }
+  }
+  if (!t1 && in_range(a, 10)) {  // slot 10: S2, holder -> straggler leader
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      if (!have) v[l] = ld_in<D, W>(hr(l, pp - 1, 0), e[l]);
+      st_fin<D, W>(sr(0), e[l], v[l]);
+    }
+    have = true;
+  }
+  if (!t1 && in_range(a, 11)) {  // slot 11: N2 distribute on the straggler server
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+      if (!have) v[l] = ld_in<D, W>(sr(0), e[l]);
+    for (int d = 1; d < g; ++d) {
+#pragma unroll
+      for (int l = 0; l < L; ++l) st_fin<D, W>(sr(d), e[l], v[l]);
+    }
+  }
+}
+
 // Section index of the quantum u of a segment's ring part.
 __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
   const uint32_t u = (uint32_t)u64;  // quanta within one segment fit in 32 bits
@@ -349,16 +574,17 @@ __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
   return sd.nbig + (int)((u - big) / (uint32_t)sd.qbase);
 }
 
-template <class D, int W, int L, int B>
+template <class D, int W, int L, int B, bool S>
 __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const SegDesc &sd,
                                           bool p2p, const int64_t (&e)[L]) {
-  if (p2p) {
+  if (!S && p2p) {
     p2p_lane<D, W, L, B>(a, rp, e);
   } else {
     int j[L];
 #pragma unroll
     for (int l = 0; l < L; ++l) j[l] = section_of(sd, (e[l] - sd.ring_begin) / kQuantum);
-    ring_lane<D, W, L, B>(a, rp, sd, j, e);
+    if constexpr (S) server_lane<D, W, L, B>(a, rp, sd, j, e);
+    else ring_lane<D, W, L, B>(a, rp, sd, j, e);
   }
 }
 
@@ -367,12 +593,16 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
 // at a stride of one workgroup-width, in lockstep; vectors past the tile's
 // last whole group go one at a time, and elements past the last whole vector
 // (only at the end of the rank vectors) one by one.
-template <class D, int W, int L>
+//
+// S selects the several-GPUs-per-server lane (App. E); its plans have no
+// point-to-point chunks.
+template <class D, int W, int L, bool S>
 __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
   constexpr int B = kHopWindow;
   constexpr int64_t kStride = (int64_t)kThreads * W;
   __shared__ void *rp[kMaxRanks];
-  for (int i = threadIdx.x; i < a.pp; i += kThreads) rp[i] = a.ptr[i];
+  const int nrp = S ? (a.pp + 1) * a.g : a.pp;  // pointers the lanes index from LDS
+  for (int i = threadIdx.x; i < nrp; i += kThreads) rp[i] = a.ptr[i];
   __syncthreads();
   // Workgroups are dealt to the XCDs round robin by workgroup index.  With
   // xcd_runs, workgroup t0 takes tile (t0 mod X) * per + t0 / X, so each XCD
@@ -393,16 +623,16 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
       int64_t e[L];
 #pragma unroll
       for (int l = 0; l < L; ++l) e[l] = e0 + l * kStride;
-      run_elems<D, W, L, B>(a, rp, sd, p2p, e);
+      run_elems<D, W, L, B, S>(a, rp, sd, p2p, e);
     }
     for (; e0 < end; e0 += kStride) {
       if (e0 + W <= end) {
         const int64_t e[1] = {e0};
-        run_elems<D, W, 1, B>(a, rp, sd, p2p, e);
+        run_elems<D, W, 1, B, S>(a, rp, sd, p2p, e);
       } else {
         for (int64_t x = e0; x < end; ++x) {
           const int64_t e[1] = {x};
-          run_elems<D, 1, 1, B>(a, rp, sd, p2p, e);
+          run_elems<D, 1, 1, B, S>(a, rp, sd, p2p, e);
         }
       }
     }

@@ -50,10 +50,87 @@ int ring_at(const optcc_plan_t &pl, int j, int t) {
   return pl.ring[(size_t)(((j + t) % pp + pp) % pp)];
 }
 
+// Several GPUs per server (App. E): rank of local ring position d (0 = the
+// part's leader) on server sv.
+int srank(const optcc_plan_t &pl, int sv, int part, int d) { return sv * pl.g + (part + d) % pl.g; }
+
+// Steps of a several-GPUs-per-server plan in execution order: slot, segment,
+// section, hop (App. E, NVLink phases N1-N4 around Stages S1-S4).  Type 1 =
+// S1-S2-S3-S4 with the straggler folding along its local ring; type 2 =
+// S3-S1-S4-S2 with plain collect and distribute on the straggler.
+template <class Fn>
+void for_each_server_step(const optcc_plan_t &pl, Fn &&fn) {
+  const int pp = pl.pp, g = pl.g, sv = pl.strag[0];
+  int src[1];
+  for (int slot = 0; slot < OPTCC_NUM_SERVER_SLOTS; ++slot) {
+    for (int gs = 0; gs < pl.nseg; ++gs) {
+      const Segment &s = pl.seg[(size_t)gs];
+      const int part = s.part;
+      const bool t1 = s.ordering == 1;
+      auto loc = [&](int server, int d) { return srank(pl, server, part, d); };
+      for (int j = 0; j < pp; ++j) {
+        int64_t b, e;
+        section_range(pl, s, j, &b, &e);
+        if (e <= b) continue;
+        auto lead = [&](int t) { return loc(ring_at(pl, j, t), 0); };
+        const int holder = lead(pp - 1);
+        auto step = [&](int op, int dst, int from) {
+          src[0] = from;
+          fn(slot, gs, j, op, dst, src, 1, b, e - b);
+        };
+        switch (slot) {
+          case 0:  // N3 collect onto the straggler's leader (type 2)
+            if (!t1) for (int d = g - 2; d >= 0; --d) step(1, loc(sv, d), loc(sv, d + 1));
+            break;
+          case 1:  // N1 collect onto every healthy leader
+            for (int h = 0; h < pp; ++h)
+              for (int d = g - 2; d >= 0; --d) step(1, loc(pl.ring[(size_t)h], d), loc(pl.ring[(size_t)h], d + 1));
+            break;
+          case 2:  // S3 (type 2): straggler's sum into the chain start
+            if (!t1) step(1, lead(0), loc(sv, 0));
+            break;
+          case 3:  // S1 chain over the healthy leaders
+            for (int t = 1; t < pp; ++t) step(1, lead(t), lead(t - 1));
+            break;
+          case 4:  // S2 (type 1): straggler leader adds the holder's partial
+            if (t1) step(1, loc(sv, 0), holder);
+            break;
+          case 5:  // N2 (type 1): fold forward along the straggler's ring
+            if (t1) for (int d = 1; d < g; ++d) step(1, loc(sv, d), loc(sv, d - 1));
+            break;
+          case 6:  // N3 (type 1): global sum back to the leader
+            if (t1) for (int d = g - 2; d >= 0; --d) step(0, loc(sv, d), loc(sv, d + 1));
+            break;
+          case 7:  // S3 (type 1): straggler leader -> holder
+            if (t1) step(0, holder, loc(sv, 0));
+            break;
+          case 8:  // S4 allgather from the holder
+            for (int t = 0; t + 1 < pp; ++t) step(0, lead(t), lead(t - 1));
+            break;
+          case 9:  // N4 distribute on every healthy server
+            for (int h = 0; h < pp; ++h)
+              for (int d = 1; d < g; ++d) step(0, loc(pl.ring[(size_t)h], d), loc(pl.ring[(size_t)h], d - 1));
+            break;
+          case 10:  // S2 (type 2): holder -> straggler leader
+            if (!t1) step(0, loc(sv, 0), holder);
+            break;
+          case 11:  // N2 (type 2): distribute on the straggler server
+            if (!t1) for (int d = 1; d < g; ++d) step(0, loc(sv, d), loc(sv, d - 1));
+            break;
+        }
+      }
+    }
+  }
+}
+
 // Visit every step in execution order: slot, segment, section (then the
 // point-to-point chunk), hop.  fn(slot, seg, sec, op, dst, srcs, nsrc, off, len).
 template <class Fn>
 void for_each_step(const optcc_plan_t &pl, Fn &&fn) {
+  if (pl.kind == OPTCC_KIND_SERVERS) {
+    for_each_server_step(pl, fn);
+    return;
+  }
   const int pp = pl.pp;
   std::vector<int> srcs((size_t)std::max(pl.p, 1));
   for (int slot = 0; slot < OPTCC_NUM_SLOTS; ++slot) {
@@ -151,6 +228,43 @@ void lane_traffic(const optcc_plan_t &pl, int ordering, bool p2p, int sb, int se
   *stores = st;
 }
 
+// The same for one lane of a section of a several-GPUs-per-server plan
+// (schedule type 1 or 2).  Mirrors the executor's server lane.
+void server_lane_traffic(const optcc_plan_t &pl, int type, int sb, int se, int64_t *loads,
+                         int64_t *stores) {
+  auto in = [&](int q) { return sb <= q && q < se; };
+  const bool t1 = type == 1;
+  const int64_t pp = pl.pp, g = pl.g;
+  const bool i0 = !t1 && in(0), i1 = in(1), i2 = !t1 && in(2), i3 = in(3);
+  int64_t ld = 0, st = 0;
+  if (i0) { ld += g; st += g - 1; }
+  if (i1) {
+    ld += pp * g;
+    st += pp * (g - 1);
+    if (i2) { if (!i0) ld += 1; st += 1; }
+    if (i3) st += pp - 1;
+  } else if (i2 || i3) {
+    ld += 1;
+    if (i2) { ld += 1; st += 1; }
+    if (i3) { ld += pp - 1; st += pp - 1; }
+  }
+  bool have = i3;
+  if (t1) {
+    if (in(4)) { ld += have ? 1 : 2; st += 1; have = true; }
+    if (in(5)) { if (!have) ld += 1; ld += g - 1; st += g - 1; have = true; }
+    if (in(6)) { if (!have) ld += 1; st += g - 1; have = true; }
+    if (in(7)) { if (!have) ld += 1; st += 1; have = true; }
+  }
+  if (in(8)) { if (!have) ld += 1; st += pp - 1; have = true; }
+  if (in(9)) { if (!have) ld += pp; st += pp * (g - 1); }
+  if (!t1) {
+    if (in(10)) { if (!have) ld += 1; st += 1; have = true; }
+    if (in(11)) { if (!have) ld += 1; st += g - 1; }
+  }
+  *loads = ld;
+  *stores = st;
+}
+
 bool valid_bw(int p, const double *bw, std::string *why) {
   if (!bw) { *why = "link_bandwidths is NULL"; return false; }
   for (int i = 0; i < p; ++i)
@@ -202,6 +316,10 @@ extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_
     pl->p = p;
     pl->k = k;
     pl->n = N;
+    pl->g = 1;
+    pl->q = p;
+    pl->nseg = k;
+    pl->nslots = OPTCC_NUM_SLOTS;
     slowdowns(p, bw, &pl->ell, &pl->strag, &pl->ring);
     pl->m = (int)pl->strag.size();
     pl->pp = (int)pl->ring.size();
@@ -248,7 +366,7 @@ extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_
       d.qbase = (int32_t)s.qbase;
       d.nbig = (int32_t)s.nbig;
       d.ordering = s.ordering;
-      d.pad = 0;
+      d.part = 0;
       // step and flow counts per non-empty section / chunk
       const int ns = n_side(*pl, s.ordering);
       const int fin = (pl->m >= 1 && s.ordering == 1) ? 2 : 0;  // Stage 2 + Stage 3 steps
@@ -279,6 +397,88 @@ extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_
   return OPTCC_OK;
 }
 
+extern "C" int optcc_plan_servers(int q, int g, const double *sbw, int64_t N, int k,
+                                  optcc_plan_t **out) {
+  set_error("");
+  if (!out) return fail(OPTCC_EINVAL, "out is NULL");
+  if (q < 3) return fail(OPTCC_EINVAL, "q must be >= 3 servers");
+  if (g < 2 || g > OPTCC_MAX_GPUS_PER_SERVER)
+    return fail(OPTCC_EINVAL, "g must be in [2, OPTCC_MAX_GPUS_PER_SERVER] (g = 1 is optcc_plan)");
+  if ((int64_t)q * g > OPTCC_MAX_RANKS) return fail(OPTCC_EUNSUPPORTED, "q*g exceeds OPTCC_MAX_RANKS");
+  if (N < 0 || N > ((int64_t)1 << 46)) return fail(OPTCC_EINVAL, "N must be in [0, 2^46]");
+  if (k < 24 || k % 8 != 0 || k > (1 << 20))
+    return fail(OPTCC_EINVAL, "n_chunks must be a multiple of 8 in [24, 2^20] (App. E)");
+  std::string why;
+  if (!valid_bw(q, sbw, &why)) return fail(OPTCC_EINVAL, why);
+  optcc_plan_t *pl = new (std::nothrow) optcc_plan_t();
+  if (!pl) return fail(OPTCC_ENOMEM, "out of host memory");
+  try {
+    const int p = q * g;
+    pl->p = p;
+    pl->g = g;
+    pl->q = q;
+    pl->k = k;
+    pl->n = N;
+    pl->nseg = g * k;
+    pl->nslots = OPTCC_NUM_SERVER_SLOTS;
+    pl->kind = OPTCC_KIND_SERVERS;
+    std::vector<double> sell;
+    slowdowns(q, sbw, &sell, &pl->strag, &pl->ring);
+    pl->m = (int)pl->strag.size();
+    pl->pp = (int)pl->ring.size();
+    if (pl->m != 1) {
+      delete pl;
+      return fail(OPTCC_EUNSUPPORTED, "exactly one straggler server is supported (App. E)");
+    }
+    pl->ell.assign((size_t)p, 1.0);
+    for (int r = 0; r < p; ++r) pl->ell[(size_t)r] = sell[(size_t)(r / g)];
+    const int64_t nq = (N + kQuantum - 1) / kQuantum;
+    pl->seg.resize((size_t)pl->nseg);
+    pl->segdesc.resize((size_t)pl->nseg);
+    int64_t steps = 0;
+    for (int part = 0; part < g; ++part) {
+      const int64_t p0 = (int64_t)((__int128)part * nq / g);
+      const int64_t lp = (int64_t)((__int128)(part + 1) * nq / g) - p0;
+      for (int c = 0; c < k; ++c) {
+        const int gs = part * k + c;
+        const int64_t q0 = p0 + (int64_t)((__int128)c * lp / k);
+        const int64_t q1 = p0 + (int64_t)((__int128)(c + 1) * lp / k);
+        Segment &s = pl->seg[(size_t)gs];
+        s.begin = std::min(q0 * kQuantum, N);
+        s.end = std::min(q1 * kQuantum, N);
+        s.ring_begin = q0 * kQuantum;
+        s.ring_end = s.end;
+        s.p2p_begin = s.p2p_end = s.end;
+        s.qbase = (q1 - q0) / pl->pp;
+        s.nbig = (q1 - q0) % pl->pp;
+        s.ordering = (c % 4 == 0 || c % 4 == 2) ? 1 : 2;  // A, C: type 1; B, D: type 2
+        s.part = part;
+        SegDesc &d = pl->segdesc[(size_t)gs];
+        d.ring_begin = s.ring_begin;
+        d.p2p_begin = s.p2p_begin;
+        d.qbase = (int32_t)s.qbase;
+        d.nbig = (int32_t)s.nbig;
+        d.ordering = s.ordering;
+        d.part = part;
+        int64_t nonempty = 0;
+        for (int j = 0; j < pl->pp; ++j) {
+          int64_t b, e;
+          section_range(*pl, s, j, &b, &e);
+          nonempty += e > b;
+        }
+        steps += nonempty * 2 * (p - 1);  // every step has one source
+      }
+    }
+    pl->num_steps = steps;
+    pl->num_flows = steps;
+  } catch (const std::bad_alloc &) {
+    delete pl;
+    return fail(OPTCC_ENOMEM, "out of host memory");
+  }
+  *out = pl;
+  return OPTCC_OK;
+}
+
 extern "C" int optcc_plan_info(const optcc_plan_t *pl, optcc_plan_info_t *info, int32_t *ring,
                                int32_t *strag, double *ell) {
   if (!pl || !info) return fail(OPTCC_EINVAL, "plan and info must be non-NULL");
@@ -291,6 +491,10 @@ extern "C" int optcc_plan_info(const optcc_plan_t *pl, optcc_plan_info_t *info, 
   info->n = pl->n;
   info->num_steps = pl->num_steps;
   info->num_flows = pl->num_flows;
+  info->g = pl->g;
+  info->q = pl->q;
+  info->num_segments = pl->nseg;
+  info->num_slots = pl->nslots;
   if (ring) for (int i = 0; i < pl->pp; ++i) ring[i] = pl->ring[(size_t)i];
   if (strag) for (int i = 0; i < pl->m; ++i) strag[i] = pl->strag[(size_t)i];
   if (ell) for (int i = 0; i < pl->p; ++i) ell[i] = pl->ell[(size_t)i];
@@ -300,7 +504,7 @@ extern "C" int optcc_plan_info(const optcc_plan_t *pl, optcc_plan_info_t *info, 
 extern "C" int optcc_plan_segments(const optcc_plan_t *pl, int64_t *off, int64_t *len,
                                    int64_t *p2p) {
   if (!pl || !off || !len || !p2p) return fail(OPTCC_EINVAL, "NULL argument");
-  for (int g = 0; g < pl->k; ++g) {
+  for (int g = 0; g < pl->nseg; ++g) {
     const Segment &s = pl->seg[(size_t)g];
     off[g] = s.begin;
     len[g] = s.end - s.begin;
@@ -344,10 +548,14 @@ extern "C" double optcc_model_time(const optcc_plan_t *pl, const double *bw) {
   if (!pl) { set_error("plan is NULL"); return NAN; }
   std::vector<double> ell = pl->ell;
   if (bw) {
+    // one bandwidth per rank, or per server for a several-GPUs-per-server plan
+    const int nb = pl->kind == OPTCC_KIND_SERVERS ? pl->q : pl->p;
     std::string why;
-    if (!valid_bw(pl->p, bw, &why)) { set_error(why); return NAN; }
+    if (!valid_bw(nb, bw, &why)) { set_error(why); return NAN; }
     std::vector<int> strag, ring;
-    slowdowns(pl->p, bw, &ell, &strag, &ring);
+    std::vector<double> e1;
+    slowdowns(nb, bw, &e1, &strag, &ring);
+    for (int i = 0; i < pl->p; ++i) ell[(size_t)i] = e1[(size_t)(i / pl->g)];
     bool same = strag == pl->strag;
     for (int i = 0; same && i < pl->p; ++i)
       same = std::fabs(ell[(size_t)i] - pl->ell[(size_t)i]) <= 1e-12 * pl->ell[(size_t)i];
@@ -357,6 +565,11 @@ extern "C" double optcc_model_time(const optcc_plan_t *pl, const double *bw) {
     }
   }
   const double p = pl->p, n = (double)pl->n, k = pl->k, m = pl->m;
+  if (pl->kind == OPTCC_KIND_SERVERS) {
+    // App. E time analysis: k + 5.5 bodies of max{l, 2} (q-1) s = max{l, 2} n/(g k)
+    const double l = ell[(size_t)(pl->strag[0] * pl->g)];
+    return std::max(l, 2.0) * n * (k + 5.5) / ((double)pl->g * k);
+  }
   switch (pl->kind) {
     case OPTCC_KIND_RING:
       return 2.0 * (p - 1.0) * n / p;  // T0 (Sec. 3)
@@ -395,24 +608,47 @@ extern "C" double optcc_lower_bound(int p, const double *bw, int64_t N) {
   return std::max(2.0 * (P - 1.0) / (P - (double)m + inv), l1) * n;
 }
 
+extern "C" double optcc_lower_bound_servers(int q, int g, const double *bw, int64_t N) {
+  if (q < 3 || g < 1 || (int64_t)q * g > OPTCC_MAX_RANKS) {
+    set_error("need q >= 3, g >= 1 and q*g <= OPTCC_MAX_RANKS");
+    return NAN;
+  }
+  if (N < 0) { set_error("N must be >= 0"); return NAN; }
+  std::string why;
+  if (!valid_bw(q, bw, &why)) { set_error(why); return NAN; }
+  std::vector<double> ell;
+  std::vector<int> strag, ring;
+  slowdowns(q, bw, &ell, &strag, &ring);
+  const double n = (double)N, Q = q, G = g, P = Q * G;
+  if (strag.empty()) return 2.0 * (P - 1.0) * n / (G * P);  // fault-free optimum (Sec. 3)
+  if (strag.size() > 1) { set_error("more than one straggler server: no bound stated"); return NAN; }
+  const double l = ell[(size_t)strag[0]];
+  return n / G * std::max(2.0 * l * (Q - 1.0) / (l * (Q - 2.0) + 2.0), l);  // App. B.3
+}
+
 extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, int sb, int se,
                                   int launches, int64_t *rd, int64_t *wr) {
   if (!pl || !rd || !wr) return fail(OPTCC_EINVAL, "NULL argument");
   if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
     return fail(OPTCC_EINVAL, "unknown dtype");
-  if (sb < 0 || se > OPTCC_NUM_SLOTS || sb > se) return fail(OPTCC_EINVAL, "bad slot range");
+  if (sb < 0 || se > pl->nslots || sb > se) return fail(OPTCC_EINVAL, "bad slot range");
+  if (launches != 0 && launches != 1) return fail(OPTCC_EINVAL, "launches must be 0 or 1");
   const int64_t es = dtype == OPTCC_BF16 ? 2 : 4;
   int64_t r = 0, w = 0;
+  auto lane = [&](int ord, bool p2p, int b, int e, int64_t *l, int64_t *s) {
+    if (pl->kind == OPTCC_KIND_SERVERS) server_lane_traffic(*pl, ord, b, e, l, s);
+    else lane_traffic(*pl, ord, p2p, b, e, l, s);
+  };
   auto add = [&](int ord, bool p2p, int64_t len) {
     if (launches == 1) {
       int64_t l, s;
-      lane_traffic(*pl, ord, p2p, sb, se, &l, &s);
+      lane(ord, p2p, sb, se, &l, &s);
       r += l * len;
       w += s * len;
     } else {
       for (int q = sb; q < se; ++q) {
         int64_t l, s;
-        lane_traffic(*pl, ord, p2p, q, q + 1, &l, &s);
+        lane(ord, p2p, q, q + 1, &l, &s);
         r += l * len;
         w += s * len;
       }
@@ -438,6 +674,9 @@ extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, i
 //    sends only data it holds); a step finishes with its last flow;
 //  * list scheduling: whenever ports free up, ready flows are started in
 //    flow order (slot, segment, section, hop) if both their ports are free.
+// Several GPUs per server (App. E bandwidth model): a flow between two GPUs of
+// one server runs over NVLink, on separate NVLink send/receive ports, at
+// (g-1) times NIC speed (len/(g-1)); flows between servers use the NICs.
 // Times are doubles; events closer than 1e-9 of the current time are merged.
 extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double *finish,
                                    int64_t cap, double *makespan) {
@@ -447,7 +686,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     return fail(OPTCC_EUNSUPPORTED, "timeline limited to 2^26 flows");
   try {
     // steps and flows in execution order
-    std::vector<int32_t> st_dst, f_src;
+    std::vector<int32_t> st_dst, f_src, f_dst;  // flows: send and receive port ids
     std::vector<int64_t> st_first, f_step;
     std::vector<double> f_dur;
     std::vector<std::vector<int64_t>> deps;
@@ -470,9 +709,13 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
       dep(dst);
       deps.push_back(std::move(d));
       for (int i = 0; i < ns; ++i) {
-        f_src.push_back(srcs[i]);
+        // port 2r: rank r's NIC; port 2r+1: its NVLink lane (same server only)
+        const bool nvl = pl->g > 1 && srcs[i] / pl->g == dst / pl->g;
+        f_src.push_back(2 * srcs[i] + (nvl ? 1 : 0));
+        f_dst.push_back(2 * dst + (nvl ? 1 : 0));
         f_step.push_back(sid);
-        f_dur.push_back((double)len * std::max(pl->ell[(size_t)srcs[i]], pl->ell[(size_t)dst]));
+        f_dur.push_back(nvl ? (double)len / (double)(pl->g - 1)
+                            : (double)len * std::max(pl->ell[(size_t)srcs[i]], pl->ell[(size_t)dst]));
       }
       last_writer[key(dst, g, sec)] = sid;
     });
@@ -485,7 +728,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
       left[(size_t)s] = (int32_t)(st_first[(size_t)s + 1] - st_first[(size_t)s]);
       for (int64_t d : deps[(size_t)s]) dependents[(size_t)d].push_back(s);
     }
-    const int p = pl->p;
+    const int p = 2 * pl->p;  // ports
     std::vector<double> fs((size_t)nfl, -1.0), ff((size_t)nfl, -1.0);
     std::vector<char> send_busy((size_t)p, 0), recv_busy((size_t)p, 0);
     // Ready flows by (sender, receiver).  Flows of one pair share both ports,
@@ -497,9 +740,8 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     std::vector<int64_t> cand;
     std::vector<int> freed_send, freed_recv;
     auto make_ready = [&](int64_t s) {
-      const int b = st_dst[(size_t)s];
       for (int64_t f = st_first[(size_t)s]; f < st_first[(size_t)s + 1]; ++f) {
-        const int a = f_src[(size_t)f];
+        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
         out_ready[(size_t)a][b].insert(f);
         in_partners[(size_t)b].insert(a);
         cand.push_back(f);
@@ -524,7 +766,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
       cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
       for (int64_t f : cand) {
         if (fs[(size_t)f] >= 0.0) continue;
-        const int a = f_src[(size_t)f], b = st_dst[(size_t)f_step[(size_t)f]];
+        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
         if (send_busy[(size_t)a] || recv_busy[(size_t)b]) continue;
         auto &q = out_ready[(size_t)a][b];
         if (q.empty() || *q.begin() != f) continue;  // an earlier flow of the pair is waiting
@@ -548,7 +790,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
         ev.pop();
         ++done;
         last = std::max(last, ff[(size_t)f]);
-        const int a = f_src[(size_t)f], b = st_dst[(size_t)f_step[(size_t)f]];
+        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
         send_busy[(size_t)a] = 0;
         recv_busy[(size_t)b] = 0;
         freed_send.push_back(a);

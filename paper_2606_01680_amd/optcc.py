@@ -17,23 +17,27 @@ LIB_PATH = os.path.join(_PKG, "liboptcc.so")
 
 OPTCC_OK, OPTCC_EINVAL, OPTCC_ENOMEM, OPTCC_EUNSUPPORTED, OPTCC_EDEVICE = 0, -1, -2, -3, -4
 OPTCC_NUM_SLOTS = 6
+OPTCC_NUM_SERVER_SLOTS = 12
+OPTCC_MAX_GPUS_PER_SERVER = 64
 OPTCC_QUANTUM = 64
 OPTCC_MAX_EMULATE_RANKS = 256
 DTYPES = {"f32": 0, "bf16": 1, "i32": 2}
-KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi"}
+KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi", 4: "servers"}
 
-EXPORTED = ("optcc_plan", "optcc_plan_free", "optcc_allreduce_emulate",
+EXPORTED = ("optcc_plan", "optcc_plan_servers", "optcc_plan_free", "optcc_allreduce_emulate",
             "optcc_allreduce_emulate_slots", "optcc_model_time", "optcc_lower_bound",
-            "optcc_last_error", "optcc_plan_info", "optcc_plan_segments",
-            "optcc_plan_num_flows", "optcc_plan_get_flows", "optcc_plan_traffic",
-            "optcc_plan_timeline")
+            "optcc_lower_bound_servers", "optcc_last_error", "optcc_plan_info",
+            "optcc_plan_segments", "optcc_plan_num_flows", "optcc_plan_get_flows",
+            "optcc_plan_traffic", "optcc_plan_timeline")
 
 
 class PlanInfo(ctypes.Structure):
     _fields_ = [("p", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("healthy", ctypes.c_int32),
                 ("quantum", ctypes.c_int32), ("n", ctypes.c_int64),
-                ("num_steps", ctypes.c_int64), ("num_flows", ctypes.c_int64)]
+                ("num_steps", ctypes.c_int64), ("num_flows", ctypes.c_int64),
+                ("g", ctypes.c_int32), ("q", ctypes.c_int32),
+                ("num_segments", ctypes.c_int32), ("num_slots", ctypes.c_int32)]
 
 
 FLOW_DTYPE = np.dtype([("slot", np.int32), ("segment", np.int32), ("section", np.int32),
@@ -54,6 +58,10 @@ def _load():
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     L.optcc_plan.argtypes = [i32, vp, i64, i32, ctypes.POINTER(vp)]
     L.optcc_plan.restype = i32
+    L.optcc_plan_servers.argtypes = [i32, i32, vp, i64, i32, ctypes.POINTER(vp)]
+    L.optcc_plan_servers.restype = i32
+    L.optcc_lower_bound_servers.argtypes = [i32, i32, vp, i64]
+    L.optcc_lower_bound_servers.restype = dbl
     L.optcc_plan_free.argtypes = [vp]
     L.optcc_plan_free.restype = None
     L.optcc_allreduce_emulate.argtypes = [vp, i32, i64, i32, vp, vp]
@@ -117,6 +125,8 @@ class Plan:
         self.kind = KINDS[info.kind]
         self.healthy, self.n = info.healthy, info.n
         self.num_steps, self.num_flows = info.num_steps, info.num_flows
+        self.g, self.q = info.g, info.q
+        self.num_segments, self.num_slots = info.num_segments, info.num_slots
         ring = np.zeros(max(self.healthy, 1), np.int32)
         strag = np.zeros(max(self.m, 1), np.int32)
         ell = np.zeros(self.p, np.float64)
@@ -131,9 +141,9 @@ class Plan:
         return self._h
 
     def segments(self):
-        off = np.zeros(self.k, np.int64)
-        ln = np.zeros(self.k, np.int64)
-        p2p = np.zeros(self.k, np.int64)
+        off = np.zeros(self.num_segments, np.int64)
+        ln = np.zeros(self.num_segments, np.int64)
+        p2p = np.zeros(self.num_segments, np.int64)
         _check(_lib.optcc_plan_segments(self._h, off.ctypes.data, ln.ctypes.data, p2p.ctypes.data))
         return off, ln, p2p
 
@@ -144,7 +154,8 @@ class Plan:
         assert got == n
         return out[:n]
 
-    def traffic(self, dtype: str, slot_begin=0, slot_end=OPTCC_NUM_SLOTS, launches=1):
+    def traffic(self, dtype: str, slot_begin=0, slot_end=None, launches=1):
+        slot_end = self.num_slots if slot_end is None else slot_end
         r, w = ctypes.c_int64(), ctypes.c_int64()
         _check(_lib.optcc_plan_traffic(self._h, DTYPES[dtype], slot_begin, slot_end, launches,
                                        ctypes.byref(r), ctypes.byref(w)))
@@ -171,6 +182,15 @@ def optcc_plan(p: int, link_bandwidths, N: int, n_chunks: int) -> Plan:
     bw = _f64(link_bandwidths, p)
     h = ctypes.c_void_p()
     _check(_lib.optcc_plan(int(p), bw.ctypes.data, int(N), int(n_chunks), ctypes.byref(h)))
+    return Plan(h)
+
+
+def optcc_plan_servers(q: int, g: int, server_bandwidths, N: int, n_chunks: int) -> Plan:
+    """q servers of g GPUs each (ranks server-major), one bandwidth per server."""
+    bw = _f64(server_bandwidths, q)
+    h = ctypes.c_void_p()
+    _check(_lib.optcc_plan_servers(int(q), int(g), bw.ctypes.data, int(N), int(n_chunks),
+                                   ctypes.byref(h)))
     return Plan(h)
 
 
@@ -232,7 +252,9 @@ def optcc_allreduce_emulate_slots(bufs, p: int, N: int, dtype: str, plan: Plan, 
 
 
 def optcc_model_time(plan: Plan, link_bandwidths=None) -> float:
-    bw = None if link_bandwidths is None else _f64(link_bandwidths, plan.p)
+    """link_bandwidths: one per rank, or one per server for a server plan."""
+    nb = plan.q if plan.kind == "servers" else plan.p
+    bw = None if link_bandwidths is None else _f64(link_bandwidths, nb)
     t = _lib.optcc_model_time(plan.handle, None if bw is None else bw.ctypes.data)
     if math.isnan(t):
         raise OptccError(OPTCC_EINVAL, optcc_last_error())
@@ -244,6 +266,14 @@ def optcc_lower_bound(p: int, link_bandwidths, N: int) -> float:
     if bw.shape != (p,):
         raise ValueError("need one bandwidth per rank")
     t = _lib.optcc_lower_bound(int(p), bw.ctypes.data, int(N))
+    if math.isnan(t):
+        raise OptccError(OPTCC_EINVAL, optcc_last_error())
+    return t
+
+
+def optcc_lower_bound_servers(q: int, g: int, server_bandwidths, N: int) -> float:
+    bw = _f64(server_bandwidths, q)
+    t = _lib.optcc_lower_bound_servers(int(q), int(g), bw.ctypes.data, int(N))
     if math.isnan(t):
         raise OptccError(OPTCC_EINVAL, optcc_last_error())
     return t

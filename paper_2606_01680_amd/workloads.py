@@ -22,13 +22,18 @@ ESIZE = {"f32": 4, "bf16": 2, "i32": 4}
 class Workload:
     name: str
     index: int          # seed block
-    p: int
-    bandwidths: tuple   # one entry per rank, healthy = 1.0
+    p: int              # ranks (q servers x g GPUs when g > 1)
+    bandwidths: tuple   # one entry per rank (per server when g > 1), healthy = 1.0
     n: int              # elements per rank
-    k: int              # segments ("n_chunks")
+    k: int              # segments ("n_chunks"; per part when g > 1)
     dtype: str
     values: str         # value recipe, see make_inputs
     note: str = field(default="", compare=False)
+    g: int = 1          # GPUs per server
+
+    @property
+    def q(self) -> int:
+        return self.p // self.g
 
 
 def _bw(p, slow):
@@ -52,6 +57,14 @@ WORKLOADS = {
     "p128_f32": Workload("p128_f32", 4, 128,
                          _bw(128, {124: 0.875, 125: 0.75, 126: 0.5, 127: 0.5}), 1 << 24, 256,
                          "f32", "student_t3_1e-3", "four stragglers"),
+    # several GPUs per server (App. E), like the paper's g = 4 experiments:
+    # the straggler server loses 4 of its 8 NICs (l = 2) or 1 of 8 (l = 8/7)
+    "q16g4_f32": Workload("q16g4_f32", 5, 64, _bw(16, {15: 0.5}), 1 << 24, 32, "f32", "normal",
+                          "16 servers x 4 GPUs, server 15 at 50% bandwidth", g=4),
+    "q32g4_f32": Workload("q32g4_f32", 6, 128, _bw(32, {31: 0.875}), 1 << 24, 32, "f32",
+                          "normal", "32 servers x 4 GPUs, server 31 lost 1 of 8 NICs", g=4),
+    "q4g4_bf16": Workload("q4g4_bf16", 7, 16, _bw(4, {0: 0.5}), 1 << 26, 32, "bf16",
+                          "normal_1e-2", "4 servers x 4 GPUs, server 0 at 50% bandwidth", g=4),
 }
 
 

@@ -116,6 +116,14 @@ def test_workload_model_values(o):
     oracle's exact rationals."""
     from paper_2606_01680_amd.workloads import WORKLOADS
     for w in WORKLOADS.values():
+        if w.g > 1:  # several GPUs per server
+            pl = o.optcc_plan_servers(w.q, w.g, w.bandwidths, w.n, w.k)
+            ell = model.slowdowns(w.bandwidths)[0][0]
+            assert o.optcc_model_time(pl) / w.n == pytest.approx(
+                float(model.optcc_servers(w.q, w.g, ell, 1, w.k)), rel=1e-13)
+            assert o.optcc_lower_bound_servers(w.q, w.g, w.bandwidths, w.n) / w.n == pytest.approx(
+                float(model.lb_servers_tight(w.q, w.g, ell, 1)), rel=1e-13)
+            continue
         pl = o.optcc_plan(w.p, w.bandwidths, w.n, w.k)
         assert o.optcc_model_time(pl) / w.n == pytest.approx(
             float(model.optcc_time(w.bandwidths, 1, w.k)), rel=1e-13)

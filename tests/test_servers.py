@@ -1,0 +1,246 @@
+"""Several GPUs per server (App. E): host rows against the oracle, and the
+HIP executor against the oracle bit for bit.
+
+The library's server plan must equal the oracle's independently built
+schedule step for step (slot, segment, section, operation, destination,
+source, range); its model time and lower bound must equal the oracle's exact
+rationals.  On the GPU every element of every rank must equal the oracle's
+serial execution, after the whole AllReduce and after every prefix of the
+twelve stage slots (fused or one launch per slot).
+"""
+import ctypes
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import model
+from test_plan_parity import _steps_of_flows
+
+
+@pytest.fixture(scope="module")
+def o():
+    from paper_2606_01680_amd import optcc
+    return optcc
+
+
+def _sbw(q, slow):
+    b = [1.0] * q
+    for s, v in slow.items():
+        b[s] = v
+    return b
+
+
+# (q, g, {straggler server: bandwidth})
+PROFILES = [
+    (3, 2, {2: 0.5}), (3, 2, {0: 0.875}), (4, 4, {1: 0.875}), (5, 3, {0: 0.5}), (3, 8, {2: 0.25}),
+    (4, 2, {3: 0.5000001}), (6, 5, {2: 0.75}), (16, 4, {15: 0.5}), (32, 4, {31: 0.875}),
+    (64, 4, {7: 0.5}),
+]
+SIZES = [(0, 24), (1, 24), (63, 24), (64 * 7 + 5, 32), (5000, 24), (64 * 24 * 3 * 2 + 17, 48)]
+
+
+@pytest.mark.parametrize("q,g,slow", PROFILES)
+@pytest.mark.parametrize("n,k", SIZES)
+def test_server_plan_equals_oracle(o, q, g, slow, n, k):
+    bw = _sbw(q, slow)
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    ref = oracle.Schedule.servers(q, g, bw, n, k)
+    assert pl.kind == "servers" == ref.kind
+    assert (pl.p, pl.g, pl.q, pl.m, pl.healthy) == (q * g, g, q, 1, q - 1)
+    assert pl.num_segments == g * k == ref.nseg and pl.num_slots == 12
+    assert list(pl.ring) == list(ref.ring) and list(pl.stragglers) == list(ref.stragglers)
+    assert np.array_equal(pl.slowdowns, ref.ell)
+    off, ln, p2p = pl.segments()
+    assert np.array_equal(off, ref.seg_off) and np.array_equal(ln, ref.seg_len)
+    assert not p2p.any()
+    fl = pl.flows()
+    assert len(fl) == pl.num_flows == pl.num_steps
+    assert _steps_of_flows(fl) == ref.steps()
+
+
+@pytest.mark.parametrize("q,g,slow", PROFILES)
+@pytest.mark.parametrize("n,k", [(1 << 20, 32), (12345, 24)])
+def test_server_model_and_bound_equal_oracle(o, q, g, slow, n, k):
+    bw = _sbw(q, slow)
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    ell = model.slowdowns(bw)[0][0]
+    t = o.optcc_model_time(pl)
+    assert t == pytest.approx(float(model.optcc_servers(q, g, ell, n, k)), rel=1e-13)
+    assert o.optcc_model_time(pl, bw) == t
+    lb = o.optcc_lower_bound_servers(q, g, bw, n)
+    assert lb == pytest.approx(float(model.lb_servers_tight(q, g, ell, n)), rel=1e-13)
+    assert t >= lb
+    # the fault-free optimum and the one-GPU bound as the g = 1 case
+    assert o.optcc_lower_bound_servers(q, g, [1.0] * q, n) == pytest.approx(
+        float(model.t0_servers(q * g, g, n)), rel=1e-13)
+    assert o.optcc_lower_bound_servers(q, 1, bw, n) == pytest.approx(
+        o.optcc_lower_bound(q, bw, n), rel=1e-13)
+
+
+def test_server_traffic(o):
+    """Fused: every input read once, one write per step: p reads and 2(p-1)
+    writes per coordinate; one launch per slot re-reads each slot's state."""
+    q, g, n = 16, 4, 1 << 20
+    pl = o.optcc_plan_servers(q, g, _sbw(q, {15: 0.5}), n, 32)
+    for dt, es in (("f32", 4), ("bf16", 2), ("i32", 4)):
+        r, w = pl.traffic(dt)
+        assert r == q * g * n * es and w == 2 * (q * g - 1) * n * es
+    r0, w0 = pl.traffic("f32", launches=0)
+    assert w0 == 2 * (q * g - 1) * n * 4 and r0 > q * g * n * 4
+
+
+def test_server_errors(o):
+    def code(*a):
+        with pytest.raises(o.OptccError) as e:
+            o.optcc_plan_servers(*a)
+        return e.value.status
+    assert code(2, 4, [1, 0.5], 100, 24) == o.OPTCC_EINVAL            # q < 3
+    assert code(4, 1, [1, 1, 1, 0.5], 100, 24) == o.OPTCC_EINVAL      # g = 1 is optcc_plan
+    assert code(4, 2, [1, 1, 1, 0.5], 100, 20) == o.OPTCC_EINVAL      # k < 24
+    assert code(4, 2, [1, 1, 1, 0.5], 100, 28) == o.OPTCC_EINVAL      # 8 does not divide k
+    assert code(4, 2, [1, 1, 1, 0.0], 100, 24) == o.OPTCC_EINVAL
+    assert code(4, 2, [1, 1, 1, 1], 100, 24) == o.OPTCC_EUNSUPPORTED  # no straggler server
+    assert code(4, 2, [1, 1, 0.5, 0.5], 100, 24) == o.OPTCC_EUNSUPPORTED
+    assert code(300, 4, [1.0] * 299 + [0.5], 100, 24) == o.OPTCC_EUNSUPPORTED
+    pl = o.optcc_plan_servers(4, 2, [1, 1, 1, 0.5], 100, 24)
+    with pytest.raises(o.OptccError):
+        o.optcc_model_time(pl, [1, 1, 0.5, 1])  # another straggler server
+    L = o.lib()
+    ptrs = (ctypes.c_void_p * 8)(*[4096 * (i + 1) for i in range(8)])
+    assert L.optcc_allreduce_emulate_slots(ptrs, 8, 100, 0, pl.handle, 0, 13, 1, None) == o.OPTCC_EINVAL
+    assert L.optcc_allreduce_emulate(ptrs, 4, 100, 0, pl.handle, None) == o.OPTCC_EINVAL
+    with pytest.raises(o.OptccError):
+        o.optcc_lower_bound_servers(4, 2, [1, 0.5, 1, 0.5], 100)
+
+
+# ------------------------------------------------------------------ GPU
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _run_both(o, q, g, slow, n, k, dtype, seed, slot_end=12, launches=1, kind="normal"):
+    torch = _gpu()
+    from gpu_util import rand_inputs, to_device, to_host
+    bw = _sbw(q, slow)
+    x = rand_inputs(dtype, q * g, n, seed, kind)
+    ref = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy(), 0, slot_end)
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    d = to_device(x, dtype)
+    o.optcc_allreduce_emulate_slots(d, q * g, n, dtype, pl, 0, slot_end, launches)
+    torch.cuda.synchronize()
+    return x, ref, to_host(d, dtype)
+
+
+GPU_PROFILES = [(3, 2, {2: 0.5}), (4, 4, {1: 0.875}), (5, 3, {0: 0.5}), (3, 8, {2: 0.25}),
+                (6, 5, {2: 0.75}), (16, 4, {15: 0.5}), (9, 3, {4: 0.875})]
+GPU_SIZES = [(1, 24), (37, 24), (2048 * 3 + 64 * 5 + 3, 24), (40000, 32)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("q,g,slow", GPU_PROFILES)
+@pytest.mark.parametrize("n,k", GPU_SIZES)
+def test_server_small_bit_exact(o, dtype, q, g, slow, n, k):
+    from gpu_util import bits_equal
+    _say(f"case servers dtype={dtype} q={q} g={g} slow={slow} n={n} k={k}")
+    x, ref, got = _run_both(o, q, g, slow, n, k, dtype, seed=q * 100 + g * 10 + n)
+    assert bits_equal(got, ref)
+    assert (got == got[0][None, :]).all()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("q,g,slow", [(3, 2, {2: 0.5}), (4, 3, {1: 0.875}), (5, 4, {0: 0.5})])
+@pytest.mark.parametrize("launches", [1, 0])
+def test_server_stage_snapshots(o, dtype, q, g, slow, launches):
+    """After the first s of the twelve slots, fused or one launch per slot,
+    every buffer equals the oracle's state after the same slots: every
+    step's destination write is materialised."""
+    from gpu_util import bits_equal
+    n, k = 2048 * 2 + 64 * 7 + 5, 24
+    for s in range(1, 13):
+        _say(f"case server snapshot dtype={dtype} q={q} g={g} slots=[0,{s}) launches={launches}")
+        x, ref, got = _run_both(o, q, g, slow, n, k, dtype, seed=29 + s, slot_end=s,
+                                launches=launches)
+        assert bits_equal(got, ref), f"slots [0,{s})"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["denormal", "wide"])
+def test_server_special_values(o, dtype, kind):
+    from gpu_util import bits_equal
+    for q, g, slow in [(3, 2, {2: 0.5}), (4, 4, {1: 0.875})]:
+        _say(f"case server special {kind} dtype={dtype} q={q} g={g}")
+        x, ref, got = _run_both(o, q, g, slow, 5000, 24, dtype, seed=3, kind=kind)
+        assert bits_equal(got, ref)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+def test_server_unaligned_buffers(o, dtype):
+    """Rank buffers that are only element-aligned take the one-element path."""
+    torch = _gpu()
+    from gpu_util import bits_equal, rand_inputs, to_device, to_host
+    q, g, n, k = 4, 3, 3000, 24
+    bw = _sbw(q, {2: 0.5})
+    p = q * g
+    x = rand_inputs(dtype, p, n, 5)
+    ref = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy())
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    stride = n + 1
+    flat = torch.zeros(p * stride + 8, dtype=to_device(x[:1, :1], dtype).dtype, device="cuda:0")
+    for r in range(p):
+        flat[1 + r * stride: 1 + r * stride + n].copy_(to_device(x[r:r + 1], dtype)[0])
+    views = [flat[1 + r * stride: 1 + r * stride + n] for r in range(p)]
+    _say(f"case server unaligned dtype={dtype}")
+    o.optcc_allreduce_emulate(views, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    got = np.stack([to_host(v, dtype) for v in views])
+    assert bits_equal(got, ref)
+
+
+SERVER_WORKLOADS = ["q4g4_bf16", "q16g4_f32", "q32g4_f32"]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", SERVER_WORKLOADS)
+def test_server_workload_full_size(o, name):
+    """Full-size server workloads: all ranks identical, within the error
+    bound of the exact sum, and every element equal to the oracle's serial
+    execution."""
+    torch = _gpu()
+    from gpu_util import bits_equal, to_host
+    from paper_2606_01680_amd.workloads import WORKLOADS as W, make_inputs
+    w = W[name]
+    _say(f"case server workload {name} q={w.q} g={w.g} N={w.n} dtype={w.dtype} k={w.k}")
+    x = make_inputs(w, device="cuda:0")
+    x0 = x.clone()
+    pl = o.optcc_plan_servers(w.q, w.g, w.bandwidths, w.n, w.k)
+    o.optcc_allreduce_emulate(x, w.p, w.n, w.dtype, pl)
+    torch.cuda.synchronize()
+    iv = x.view(torch.int16) if w.dtype == "bf16" else x.view(torch.int32)
+    for r in range(1, w.p):
+        assert torch.equal(iv[r], iv[0]), r
+    step = max(1 << 16, (1 << 28) // w.p)
+    for c0 in range(0, w.n, step):
+        c1 = min(w.n, c0 + step)
+        xs = x0[:, c0:c1].to(torch.float64)
+        err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
+        u = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8
+        assert bool((err <= w.p * u * xs.abs().sum(0)).all())
+    _say(f"case server workload {name}: full oracle run")
+    full = oracle.run(oracle.Schedule.servers(w.q, w.g, w.bandwidths, w.n, w.k), w.dtype,
+                      to_host(x0, w.dtype).copy())
+    del x0
+    assert bits_equal(to_host(x, w.dtype), full)
