@@ -16,28 +16,36 @@ namespace {
 
 using namespace kern;
 
-template <class D, bool S>
+template <class D, bool S, int G>
 hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   constexpr int W16 = 16 / (int)sizeof(typename D::S);
   const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
-  if (!vec16) {
-    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S>), grid, block, 0, st, a);
+  if (!vec16) {  // element-aligned buffers: the general lane, one element per access
+    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, 0, st, a);
     return hipGetLastError();
   }
   if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
     if (two) {
-      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S, G>), grid, block, 0, st, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S>), grid, block, 0, st, a);
+  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S, G>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
+// Several GPUs per server: the usual server sizes g = 2, 4, 8 get a kernel
+// with the local ring fixed at compile time.
 template <class D>
 hipError_t launch_plan(const KArgs &a, bool servers, bool vec16, bool two, hipStream_t st) {
-  return servers ? launch<D, true>(a, vec16, two, st) : launch<D, false>(a, vec16, two, st);
+  if (!servers) return launch<D, false, 0>(a, vec16, two, st);
+  switch (a.g) {
+    case 2: return launch<D, true, 2>(a, vec16, two, st);
+    case 4: return launch<D, true, 4>(a, vec16, two, st);
+    case 8: return launch<D, true, 8>(a, vec16, two, st);
+    default: return launch<D, true, 0>(a, vec16, two, st);
+  }
 }
 
 int device_tables(const optcc_plan_t &pl, DeviceTables *out) {

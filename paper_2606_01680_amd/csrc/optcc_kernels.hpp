@@ -103,13 +103,20 @@ struct alignas(sizeof(typename D::S) * W) Vec {
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Rank buffers are device (global) memory.  Pointers read from LDS are
+// generic, which would make every access a FLAT instruction; FLAT accesses
+// count against the LDS wait counter too, so each wait for an LDS pointer
+// read would also drain every memory load in flight.  Accessing through the
+// global address space keeps the two counters apart.
+#define OPTCC_GLOBAL __attribute__((address_space(1)))
 
 // Loads and stores of W elements; NT selects the streaming hint.
 template <class D, int W, bool NT = false>
 __device__ __forceinline__ Vec<D, W> vload(const void *base, int64_t e) {
-  const typename D::S *p = static_cast<const typename D::S *>(base) + e;
+  using S = typename D::S;
+  const OPTCC_GLOBAL S *p = (const OPTCC_GLOBAL S *)base + e;
   if constexpr (sizeof(Vec<D, W>) == 16) {
-    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+    const OPTCC_GLOBAL u32x4 *q = (const OPTCC_GLOBAL u32x4 *)p;
     const u32x4 r = NT ? __builtin_nontemporal_load(q) : *q;
     return __builtin_bit_cast(Vec<D, W>, r);
   } else {
@@ -121,9 +128,10 @@ __device__ __forceinline__ Vec<D, W> vload(const void *base, int64_t e) {
 }
 template <class D, int W, bool NT = false>
 __device__ __forceinline__ void vstore(void *base, int64_t e, const Vec<D, W> &x) {
-  typename D::S *p = static_cast<typename D::S *>(base) + e;
+  using S = typename D::S;
+  OPTCC_GLOBAL S *p = (OPTCC_GLOBAL S *)base + e;
   if constexpr (sizeof(Vec<D, W>) == 16) {
-    u32x4 *q = reinterpret_cast<u32x4 *>(p);
+    OPTCC_GLOBAL u32x4 *q = (OPTCC_GLOBAL u32x4 *)p;
     const u32x4 v = __builtin_bit_cast(u32x4, x);
     if (NT) __builtin_nontemporal_store(v, q);
     else *q = v;
@@ -367,11 +375,19 @@ __device__ __forceinline__ int local_gpu(int part, int d, int g) {
   return i >= g ? i - g : i;
 }
 
-template <class D, int W, int L, int B>
+//
+// G > 0: the plan has exactly G GPUs per server (a compile-time local ring).
+// For slot ranges that start at slot 0 or 1 and reach slot 6 (the whole
+// AllReduce among them) the lane then runs on units of one server's G
+// values: the straggler server's G raw values are loaded first, the chain
+// servers' units stream through a window of about B loads, and the steady
+// state is straight-line code.  Other ranges, and G = 0, take the general
+// path below (any g, any slot range).
+template <class D, int W, int L, int B, int G>
 __device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, const SegDesc &sd, const int (&j)[L],
                             const int64_t (&e)[L]) {
   using V = Vec<D, W>;
-  const int pp = a.pp, g = a.g, part = sd.part;
+  const int pp = a.pp, g = G > 0 ? G : a.g, part = sd.part;
   const bool t1 = sd.ordering == 1;
   // buffer of chain position t (server R[j+t], 0 <= t < pp) at local position d
   auto hr = [&](int l, int t, int d) __attribute__((always_inline)) {
@@ -384,7 +400,111 @@ __device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, con
   const bool i3 = in_range(a, 3), i4 = t1 && in_range(a, 4), i5 = t1 && in_range(a, 5);
   V v[L], acc[L], ss[L];
   bool have = false;  // v holds the value the next step reads
+  bool head_done = false;
 
+  if constexpr (G > 0) {
+    if (a.sb <= 1 && a.se >= 6) {
+      constexpr int BU = B / G > 2 ? B / G : 2;  // chain units in flight
+      const bool s0 = !t1 && a.sb == 0;         // slot 0 runs
+      V xs[G][L];                               // the straggler server's raw values
+      if (s0 || t1) {
+#pragma unroll
+        for (int d = G - 1; d >= 0; --d)
+#pragma unroll
+          for (int l = 0; l < L; ++l) xs[d][l] = ld_in<D, W>(sr(d), e[l]);
+      }
+      V buf[BU][G][L];
+      auto load_unit = [&](int t, V (&x)[G][L]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int d = G - 1; d >= 0; --d)
+#pragma unroll
+          for (int l = 0; l < L; ++l) x[d][l] = ld_in<D, W>(hr(l, t, d), e[l]);
+      };
+      // slot 1: N1 collect of chain server t; acc ends as the leader's sum
+      auto collect = [&](int t, const V (&x)[G][L]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int l = 0; l < L; ++l) acc[l] = x[G - 1][l];
+#pragma unroll
+        for (int d = G - 2; d >= 0; --d)
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            acc[l] = add2<D, W>(x[d][l], acc[l]);
+            st_mid<D, W>(hr(l, t, d), e[l], acc[l]);
+          }
+      };
+      // slots 1 and 3 at chain server t >= 1
+      auto hop = [&](int t, const V (&x)[G][L]) __attribute__((always_inline)) {
+        collect(t, x);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          v[l] = add2<D, W>(acc[l], v[l]);
+          st_mid<D, W>(hr(l, t, 0), e[l], v[l]);
+        }
+      };
+#pragma unroll
+      for (int u = 0; u < BU; ++u)
+        if (u < pp) load_unit(u, buf[u]);
+      if (s0) {  // slot 0: N3 collect on the straggler server (type 2)
+#pragma unroll
+        for (int l = 0; l < L; ++l) ss[l] = xs[G - 1][l];
+#pragma unroll
+        for (int d = G - 2; d >= 0; --d)
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            ss[l] = add2<D, W>(xs[d][l], ss[l]);
+            st_mid<D, W>(sr(d), e[l], ss[l]);
+          }
+      }
+      collect(0, buf[0]);  // the chain start
+      if (!t1) {           // slot 2: S3 into the chain start (type 2)
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          const V s2 = s0 ? ss[l] : ld_in<D, W>(sr(0), e[l]);
+          v[l] = add2<D, W>(s2, acc[l]);
+          st_mid<D, W>(hr(l, 0, 0), e[l], v[l]);
+        }
+      } else {
+#pragma unroll
+        for (int l = 0; l < L; ++l) v[l] = acc[l];
+      }
+      if (BU < pp) load_unit(BU, buf[0]);
+      // chain servers t = 1 .. pp-1; unit t sits in buf[t mod BU]
+      int t0 = 1;
+      for (; t0 + 2 * BU <= pp; t0 += BU) {  // steady state: every refill exists
+#pragma unroll
+        for (int u = 0; u < BU; ++u) {
+          hop(t0 + u, buf[(1 + u) % BU]);
+          load_unit(t0 + u + BU, buf[(1 + u) % BU]);
+        }
+      }
+      for (; t0 < pp; t0 += BU) {
+#pragma unroll
+        for (int u = 0; u < BU; ++u)
+          if (t0 + u < pp) {
+            hop(t0 + u, buf[(1 + u) % BU]);
+            if (t0 + u + BU < pp) load_unit(t0 + u + BU, buf[(1 + u) % BU]);
+          }
+      }
+      if (t1) {  // slot 4: S2; slot 5: N2 fold along the straggler's ring
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          v[l] = add2<D, W>(xs[0][l], v[l]);
+          st_mid<D, W>(sr(0), e[l], v[l]);
+        }
+#pragma unroll
+        for (int d = 1; d < G; ++d)
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            v[l] = add2<D, W>(xs[d][l], v[l]);
+            if (d == G - 1) st_fin<D, W>(sr(d), e[l], v[l]);
+            else st_mid<D, W>(sr(d), e[l], v[l]);
+          }
+      }
+      have = true;
+      head_done = true;
+    }
+  }
+  if (!head_done) {
   // Slots 2/3 without slot 1 (partial slot ranges only): the leaders already
   // hold their collected values.
   if (!i1 && (i2 || i3)) {
@@ -507,6 +627,7 @@ __device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, con
     for (int l = 0; l < L; ++l) v[l] = acc[l];
     have = true;
   }
+  }  // general path
 
   if (t1 && in_range(a, 6)) {  // slot 6: N3, the global sum back to the leader
 #pragma unroll
@@ -574,7 +695,7 @@ __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
   return sd.nbig + (int)((u - big) / (uint32_t)sd.qbase);
 }
 
-template <class D, int W, int L, int B, bool S>
+template <class D, int W, int L, int B, bool S, int G>
 __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const SegDesc &sd,
                                           bool p2p, const int64_t (&e)[L]) {
   if (!S && p2p) {
@@ -583,7 +704,7 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
     int j[L];
 #pragma unroll
     for (int l = 0; l < L; ++l) j[l] = section_of(sd, (e[l] - sd.ring_begin) / kQuantum);
-    if constexpr (S) server_lane<D, W, L, B>(a, rp, sd, j, e);
+    if constexpr (S) server_lane<D, W, L, B, G>(a, rp, sd, j, e);
     else ring_lane<D, W, L, B>(a, rp, sd, j, e);
   }
 }
@@ -595,8 +716,9 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
 // (only at the end of the rank vectors) one by one.
 //
 // S selects the several-GPUs-per-server lane (App. E); its plans have no
-// point-to-point chunks.
-template <class D, int W, int L, bool S>
+// point-to-point chunks.  G: GPUs per server when fixed at compile time
+// (0: read from the arguments).
+template <class D, int W, int L, bool S, int G>
 __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
   constexpr int B = kHopWindow;
   constexpr int64_t kStride = (int64_t)kThreads * W;
@@ -623,16 +745,16 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
       int64_t e[L];
 #pragma unroll
       for (int l = 0; l < L; ++l) e[l] = e0 + l * kStride;
-      run_elems<D, W, L, B, S>(a, rp, sd, p2p, e);
+      run_elems<D, W, L, B, S, G>(a, rp, sd, p2p, e);
     }
     for (; e0 < end; e0 += kStride) {
       if (e0 + W <= end) {
         const int64_t e[1] = {e0};
-        run_elems<D, W, 1, B, S>(a, rp, sd, p2p, e);
+        run_elems<D, W, 1, B, S, G>(a, rp, sd, p2p, e);
       } else {
         for (int64_t x = e0; x < end; ++x) {
           const int64_t e[1] = {x};
-          run_elems<D, 1, 1, B, S>(a, rp, sd, p2p, e);
+          run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
         }
       }
     }

@@ -54,6 +54,14 @@ class OptccError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2606_01680_amd.build`")
+    # One HIP runtime per process: torch ships its own libamdhip64 with the
+    # same soname as the system one the library is linked against, and the
+    # first one loaded serves everybody.  Load torch first, so that the
+    # library runs on the runtime that owns torch's device memory and streams.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - plain C-ABI use without torch
+        pass
     L = ctypes.CDLL(LIB_PATH)
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     L.optcc_plan.argtypes = [i32, vp, i64, i32, ctypes.POINTER(vp)]
