@@ -19,6 +19,10 @@ Rules (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
   step order; at every event time the unstarted flows are scanned in that
   order and each one whose dependencies are done and whose two ports are free
   starts.
+* Several GPUs per server (App. E bandwidth model): a flow between two GPUs
+  of the same server uses their NVLink lanes, not their NICs: separate send
+  and receive ports per GPU, each running at (g-1) times NIC speed, so the
+  flow lasts len/(g-1).  Bandwidths are then given per server.
 
 Times are exact rationals (``fractions.Fraction``), so there are no ties to
 break by tolerance (the library, in doubles, merges events closer than 1e-9 of
@@ -36,6 +40,22 @@ def slowdowns(bandwidths):
     b = [F(x) for x in bandwidths]
     bmax = max(b)
     return [(bmax / x).limit_denominator(10**6) for x in b]
+
+
+def rank_slowdowns(sched, bandwidths):
+    """Slowdown of every rank: one bandwidth per rank, or per server when
+    the schedule has g > 1 GPUs per server."""
+    ell = slowdowns(bandwidths)
+    g = getattr(sched, "g", 1)
+    return [ell[r // g] for r in range(sched.p)] if g > 1 else ell
+
+
+def flow_cost(sched, ell, a, b, ln):
+    """(port kind, duration) of a flow of ln elements from rank a to rank b."""
+    g = getattr(sched, "g", 1)
+    if g > 1 and a // g == b // g:
+        return "nvlink", F(ln, g - 1)
+    return "nic", ln * max(ell[a], ell[b])
 
 
 def dependencies(steps):
@@ -57,18 +77,19 @@ def dependencies(steps):
 def evaluate(sched, bandwidths):
     """(makespan, [(start, finish) per flow in flow order])."""
     steps = sched.steps()
-    ell = slowdowns(bandwidths)
+    ell = rank_slowdowns(sched, bandwidths)
     deps = dependencies(steps)
     flows = []
     for i, st in enumerate(steps):
         for src in st["srcs"]:
-            flows.append((i, src, st["dst"], st["len"] * max(ell[src], ell[st["dst"]])))
+            kind, dur = flow_cost(sched, ell, src, st["dst"], st["len"])
+            flows.append((i, (kind, src), (kind, st["dst"]), dur))
     left = [len(st["srcs"]) for st in steps]
     done_steps = set()
     start = [None] * len(flows)
     finish = [None] * len(flows)
-    send_free = [F(0)] * sched.p
-    recv_free = [F(0)] * sched.p
+    send_free = {}
+    recv_free = {}
     t = F(0)
     running = []
     remaining = len(flows)
@@ -76,7 +97,7 @@ def evaluate(sched, bandwidths):
         for f, (i, a, b, dur) in enumerate(flows):
             if start[f] is not None or not deps[i] <= done_steps:
                 continue
-            if send_free[a] > t or recv_free[b] > t:
+            if send_free.get(a, F(0)) > t or recv_free.get(b, F(0)) > t:
                 continue
             start[f], finish[f] = t, t + dur
             send_free[a] = recv_free[b] = t + dur
@@ -99,28 +120,31 @@ def validate(sched, bandwidths, times):
     durations, one flow per port at a time, and data dependencies.
     Returns a list of violations (empty when valid)."""
     steps = sched.steps()
-    ell = slowdowns(bandwidths)
+    ell = rank_slowdowns(sched, bandwidths)
     deps = dependencies(steps)
     errs = []
-    flows = [(i, src, st["dst"], st["len"]) for i, st in enumerate(steps) for src in st["srcs"]]
+    flows = []
+    for i, st in enumerate(steps):
+        for src in st["srcs"]:
+            kind, dur = flow_cost(sched, ell, src, st["dst"], st["len"])
+            flows.append((i, (kind, src), (kind, st["dst"]), dur))
     if len(flows) != len(times):
         return [f"{len(times)} times for {len(flows)} flows"]
     step_end = {}
-    for (i, a, b, ln), (s, e) in zip(flows, times):
-        dur = ln * max(ell[a], ell[b])
+    for (i, a, b, dur), (s, e) in zip(flows, times):
         if abs(F(e) - F(s) - dur) > F(1, 10**6) * max(1, dur):
             errs.append(f"flow of step {i}: duration {e - s} != {dur}")
         step_end[i] = max(step_end.get(i, F(-1)), F(e))
     for port in ("send", "recv"):
         busy = {}
-        for (i, a, b, ln), (s, e) in zip(flows, times):
+        for (i, a, b, dur), (s, e) in zip(flows, times):
             busy.setdefault(a if port == "send" else b, []).append((F(s), F(e)))
         for r, iv in busy.items():
             iv.sort()
             for (s0, e0), (s1, e1) in zip(iv, iv[1:]):
                 if s1 < e0 - F(1, 10**6) * max(1, e0):
                     errs.append(f"rank {r} {port} port: overlapping flows at {s1}")
-    for (i, a, b, ln), (s, e) in zip(flows, times):
+    for (i, a, b, dur), (s, e) in zip(flows, times):
         for d in deps[i]:
             if F(s) < step_end[d] - F(1, 10**6) * max(1, step_end[d]):
                 errs.append(f"step {i} starts before its dependency {d} ends")

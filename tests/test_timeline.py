@@ -109,3 +109,58 @@ def test_workload_evaluated_times(o, w):
         assert mk <= closed * (1 + 1e-12)
     else:
         assert mk <= closed * 1.01
+
+
+# ------------------------------------------------ several GPUs per server
+# (q, g, {straggler server: bandwidth}, n, k): small enough for the naive
+# exact-rational scan, with every section of a segment non-empty in the
+# larger cases
+SERVER_CASES = [
+    (3, 2, {2: 0.5}, 64 * 48, 24), (3, 2, {0: 0.875}, 64 * 2 * 24 * 2, 24),
+    (4, 2, {1: 0.5}, 64 * 2 * 24 * 3, 24), (3, 3, {2: 0.25}, 64 * 3 * 24 * 2, 24),
+    (4, 4, {3: 0.875}, 64 * 4 * 24, 24),
+]
+
+
+def _sbw(q, slow):
+    b = [1.0] * q
+    for s, v in slow.items():
+        b[s] = v
+    return b
+
+
+@pytest.mark.parametrize("q,g,slow,n,k", SERVER_CASES)
+def test_server_timeline_equals_oracle(o, q, g, slow, n, k):
+    """App. E bandwidth model: NVLink flows on their own ports at (g-1)x NIC
+    speed, NIC flows as in the one-GPU model; the library's evaluation equals
+    the oracle's exact one flow by flow and passes the validator."""
+    bw = _sbw(q, slow)
+    sched = oracle.Schedule.servers(q, g, bw, n, k)
+    mk_ref, ref = T.evaluate(sched, bw)
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    mk, st, fi = pl.timeline()
+    scale = max(1.0, float(mk_ref))
+    assert abs(mk - float(mk_ref)) <= 1e-9 * scale
+    assert len(st) == len(ref)
+    assert np.allclose(st, [float(a) for a, _ in ref], rtol=0, atol=1e-9 * scale)
+    assert np.allclose(fi, [float(b) for _, b in ref], rtol=0, atol=1e-9 * scale)
+    assert T.validate(sched, bw, list(zip(st, fi))) == []
+    # Theorem 3 and its tight form hold for any correct AllReduce
+    ell = model.slowdowns(bw)[0][0]
+    assert mk_ref >= model.lb_servers_tight(q, g, ell, n)
+
+
+def test_server_validator_uses_nvlink_ports():
+    """An NVLink flow must last len/(g-1); a NIC flow between servers and an
+    NVLink flow of the same rank may overlap (different ports), two NVLink
+    flows of one rank may not."""
+    q, g, bw, n, k = 3, 2, [1, 1, 0.5], 64 * 48, 24
+    sched = oracle.Schedule.servers(q, g, bw, n, k)
+    _, good = T.evaluate(sched, bw)
+    assert T.validate(sched, bw, good) == []
+    flows = [(src, st["dst"]) for st in sched.steps() for src in st["srcs"]]
+    i = next(i for i, (a, b) in enumerate(flows) if a // g == b // g)
+    s, e = good[i]
+    bad = list(good)
+    bad[i] = (s, s + 2 * (e - s))  # an NVLink flow at NIC speed
+    assert any("duration" in x for x in T.validate(sched, bw, bad))
