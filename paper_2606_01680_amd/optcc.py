@@ -181,7 +181,7 @@ class Plan:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None:
+        if h is not None and _lib is not None:  # _lib is gone at interpreter exit
             _lib.optcc_plan_free(h)
             self._h = None
 

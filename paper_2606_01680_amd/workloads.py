@@ -59,11 +59,11 @@ WORKLOADS = {
                          "f32", "student_t3_1e-3", "four stragglers"),
     # several GPUs per server (App. E), like the paper's g = 4 experiments:
     # the straggler server loses 4 of its 8 NICs (l = 2) or 1 of 8 (l = 8/7)
-    "q16g4_f32": Workload("q16g4_f32", 5, 64, _bw(16, {15: 0.5}), 1 << 24, 32, "f32", "normal",
+    "q16g4_f32": Workload("q16g4_f32", 5, 64, _bw(16, {15: 0.5}), 1 << 24, 128, "f32", "normal",
                           "16 servers x 4 GPUs, server 15 at 50% bandwidth", g=4),
-    "q32g4_f32": Workload("q32g4_f32", 6, 128, _bw(32, {31: 0.875}), 1 << 24, 32, "f32",
+    "q32g4_f32": Workload("q32g4_f32", 6, 128, _bw(32, {31: 0.875}), 1 << 24, 128, "f32",
                           "normal", "32 servers x 4 GPUs, server 31 lost 1 of 8 NICs", g=4),
-    "q4g4_bf16": Workload("q4g4_bf16", 7, 16, _bw(4, {0: 0.5}), 1 << 26, 32, "bf16",
+    "q4g4_bf16": Workload("q4g4_bf16", 7, 16, _bw(4, {0: 0.5}), 1 << 26, 128, "bf16",
                           "normal_1e-2", "4 servers x 4 GPUs, server 0 at 50% bandwidth", g=4),
 }
 
