@@ -244,3 +244,42 @@ def test_server_workload_full_size(o, name):
                       to_host(x0, w.dtype).copy())
     del x0
     assert bits_equal(to_host(x, w.dtype), full)
+
+
+@pytest.mark.gpu
+def test_server_graph_capture_replays(o):
+    """A server-plan AllReduce is one kernel launch after its first call, so
+    it can be captured in a HIP graph; every replay (eager restores and
+    synchronisations in between) equals the eager result bit for bit."""
+    torch = _gpu()
+    from gpu_util import bits_equal, rand_inputs, to_device, to_host
+    q, g, n, k = 4, 4, 200000, 24
+    bw = _sbw(q, {1: 0.875})
+    p = q * g
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    for dtype in ("f32", "bf16", "i32"):
+        x = rand_inputs(dtype, p, n, 41)
+        d = to_device(x, dtype)
+        d0 = d.clone()
+        o.optcc_allreduce_emulate(d, p, n, dtype, pl)  # first use: table upload
+        torch.cuda.synchronize()
+        eager = d.clone()
+        ref = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy())
+        assert bits_equal(to_host(eager, dtype), ref)
+        gr = torch.cuda.CUDAGraph()
+        d.copy_(d0)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(gr, stream=s):
+                o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+        torch.cuda.synchronize()
+        iv = torch.int16 if dtype == "bf16" else torch.int32
+        for rep in range(3):
+            _say(f"case server graph replay dtype={dtype} rep={rep}")
+            d.copy_(d0)
+            torch.cuda.synchronize()
+            gr.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(d.view(iv), eager.view(iv))
+        del gr
