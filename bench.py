@@ -19,9 +19,10 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "achieved HBM GB/s of OptCC schedule execution (1 GPU) and % of peak BW"
 PEAK_GBPS = 8000.0  # MI355X HBM3E
-# device code of the executor (kernels and the tile/segment table layouts)
+# device code of the executor (kernels, table layouts, launch choices)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01680_amd", "csrc", f)
-               for f in ("optcc_kernels.hpp", "optcc_internal.hpp")]
+               for f in ("optcc_kernels.hpp", "optcc_internal.hpp", "optcc_launch.hpp",
+                         "optcc_exec.hip")]
 
 
 def kernel_hash() -> str:

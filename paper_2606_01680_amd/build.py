@@ -22,8 +22,11 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+KERNEL_TUS = ("optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip", "optcc_kern_i32.hip")
+
+
 def sources():
-    return [os.path.join(CSRC, f) for f in ("optcc_plan.cpp", "optcc_exec.hip")]
+    return [os.path.join(CSRC, f) for f in ("optcc_plan.cpp",) + KERNEL_TUS]
 
 
 def _run(cmd):
@@ -32,22 +35,41 @@ def _run(cmd):
 
 
 def build(verbose: bool = True) -> str:
+    """Compile every translation unit (in parallel) and link liboptcc.so."""
+    from concurrent.futures import ThreadPoolExecutor
+
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
-    plan_o = os.path.join(BUILD, "optcc_plan.o")
-    _run(["g++", *COMMON, "-c", os.path.join(CSRC, "optcc_plan.cpp"), "-o", plan_o,
-          "-I/opt/rocm/include"])
-    objs.append(plan_o)
-    exec_o = os.path.join(BUILD, "optcc_exec.o")
-    _run([HIPCC, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c",
-          os.path.join(CSRC, "optcc_exec.hip"), "-o", exec_o])
-    objs.append(exec_o)
+    jobs = [["g++", *COMMON, "-c", os.path.join(CSRC, "optcc_plan.cpp"), "-o",
+             os.path.join(BUILD, "optcc_plan.o"), "-I/opt/rocm/include"]]
+    for tu in KERNEL_TUS:
+        jobs.append([HIPCC, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c",
+                     os.path.join(CSRC, tu), "-o", os.path.join(BUILD, tu.replace(".hip", ".o"))])
+    workers = max(1, min(len(jobs), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(workers) as ex:
+        for f in [ex.submit(_run, j) for j in jobs]:
+            f.result()
+    objs = [j[j.index("-o") + 1] for j in jobs]
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
     return LIB
 
 
+C_CHECK_SRC = os.path.join(ROOT, "tests", "c_abi_check.c")
+C_CHECK = os.path.join(ROOT, "tests", "c_abi_check")
+
+
+def build_c_check() -> str:
+    """Compile the plain-C user of the C ABI (tests/c_abi_check.c) with gcc
+    against include/optcc.h, liboptcc.so and the HIP runtime."""
+    _run(["gcc", "-std=c99", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+          f"-I{INCLUDE}", C_CHECK_SRC, "-o", C_CHECK + ".tmp", f"-L{PKG}", "-loptcc",
+          "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,$ORIGIN/../paper_2606_01680_amd"])
+    os.replace(C_CHECK + ".tmp", C_CHECK)
+    return C_CHECK
+
+
 if __name__ == "__main__":
     build()
+    build_c_check()
     sys.exit(0)

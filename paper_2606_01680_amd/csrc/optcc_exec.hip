@@ -1,6 +1,6 @@
 // Host side of the OptCC executor on one MI355X (gfx950, CDNA4): argument
 // checks, the per-device plan tables and kernel launches.  The kernels are
-// in optcc_kernels.hpp.
+// in optcc_kernels.hpp, instantiated per element type in optcc_kern_*.hip.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -9,44 +9,12 @@
 #include <vector>
 
 #include "optcc_internal.hpp"
-#include "optcc_kernels.hpp"
+#include "optcc_launch.hpp"
 
 namespace optcc {
 namespace {
 
 using namespace kern;
-
-template <class D, bool S, int G>
-hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
-  constexpr int W16 = 16 / (int)sizeof(typename D::S);
-  const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
-  const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
-  if (!vec16) {  // element-aligned buffers: the general lane, one element per access
-    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, 0, st, a);
-    return hipGetLastError();
-  }
-  if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
-    if (two) {
-      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S, G>), grid, block, 0, st, a);
-      return hipGetLastError();
-    }
-  }
-  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S, G>), grid, block, 0, st, a);
-  return hipGetLastError();
-}
-
-// Several GPUs per server: the usual server sizes g = 2, 4, 8 get a kernel
-// with the local ring fixed at compile time.
-template <class D>
-hipError_t launch_plan(const KArgs &a, bool servers, bool vec16, bool two, hipStream_t st) {
-  if (!servers) return launch<D, false, 0>(a, vec16, two, st);
-  switch (a.g) {
-    case 2: return launch<D, true, 2>(a, vec16, two, st);
-    case 4: return launch<D, true, 4>(a, vec16, two, st);
-    case 8: return launch<D, true, 8>(a, vec16, two, st);
-    default: return launch<D, true, 0>(a, vec16, two, st);
-  }
-}
 
 int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
   int dev = 0;
@@ -157,9 +125,9 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     a.se = launches == 1 ? se : sb + l + 1;
     hipError_t err = hipSuccess;
     switch (dtype) {
-      case OPTCC_F32: err = launch_plan<F32>(a, servers, vec16, two, st); break;
-      case OPTCC_BF16: err = launch_plan<BF16>(a, servers, vec16, false, st); break;
-      default: err = launch_plan<I32>(a, servers, vec16, two, st); break;
+      case OPTCC_F32: err = launch_f32(a, servers, vec16, two, st); break;
+      case OPTCC_BF16: err = launch_bf16(a, servers, vec16, false, st); break;
+      default: err = launch_i32(a, servers, vec16, two, st); break;
     }
     if (err != hipSuccess)
       return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));
