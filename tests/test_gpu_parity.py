@@ -283,3 +283,61 @@ def test_graph_capture_replays(o):
             assert torch.equal(d.view(torch.int16 if dtype == "bf16" else torch.int32),
                                eager.view(torch.int16 if dtype == "bf16" else torch.int32))
         del g
+
+
+def test_every_small_length(o):
+    """Every length from 0 to 200 and around each tile and quantum boundary up
+    to three tiles, for one straggler (bubble filling), several stragglers
+    and a server plan: bit for bit against the oracle."""
+    lengths = sorted(set(range(0, 201)) | {b + d for b in (1984, 2048, 4096, 6144)
+                                           for d in (-65, -64, -63, -1, 0, 1, 63, 64, 65)})
+    profiles = [("one", 8, {7: 0.875}, None), ("multi", 9, {0: 0.875, 3: 0.75, 8: 0.5}, None),
+                ("servers", 6, None, (3, 2, [1.0, 1.0, 0.5]))]
+    for name, p, slow, srv in profiles:
+        _say(f"case every small length {name}")
+        for n in lengths:
+            x = rand_inputs("i32", p, n, 7 + n)
+            if srv is None:
+                bw = _bw(p, slow)
+                pl, sched = o.optcc_plan(p, bw, n, 8), oracle.Schedule(p, bw, n, 8)
+            else:
+                q, g, sbw = srv
+                pl = o.optcc_plan_servers(q, g, sbw, n, 24)
+                sched = oracle.Schedule.servers(q, g, sbw, n, 24)
+            ref = oracle.run(sched, "i32", x.copy())
+            d = to_device(x, "i32")
+            o.optcc_allreduce_emulate(d, p, n, "i32", pl)
+            torch.cuda.synchronize()
+            assert bits_equal(to_host(d, "i32"), ref), (name, n)
+
+
+def test_more_than_2g_elements_per_rank(o):
+    """N = 2^31 + 4099 elements per rank (three ranks, 25.8 GB): element
+    offsets beyond 32 bits.  All ranks identical, the exact wrapped int32
+    sum everywhere, and sampled coordinates (segment and section ends, the
+    last elements) bit for bit against the oracle."""
+    p, n, k = 3, (1 << 31) + 4099, 4
+    bw = [1.0, 1.0, 0.5]
+    _say(f"case p=3 N={n} i32")
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(2606)
+    x0 = torch.randint(-(1 << 30), 1 << 30, (p, n), generator=g, device="cuda:0", dtype=torch.int32)
+    x = x0.clone()
+    pl = o.optcc_plan(p, bw, n, k)
+    o.optcc_allreduce_emulate(x, p, n, "i32", pl)
+    torch.cuda.synchronize()
+    for r in range(1, p):
+        assert torch.equal(x[r], x[0]), r
+    step = 1 << 28
+    for c0 in range(0, n, step):
+        c1 = min(n, c0 + step)
+        want = x0[:, c0:c1].to(torch.int64).sum(0)
+        want = ((want + 2**31) % 2**32 - 2**31).to(torch.int32)
+        assert torch.equal(x[0, c0:c1], want), c0
+    rng = np.random.default_rng(31)
+    coords = _sample_coords(pl, n, rng, count=2048)
+    coords = np.unique(np.concatenate([coords, np.arange(n - 300, n)]))
+    idx = torch.from_numpy(coords).to("cuda:0")
+    cols = to_host(x0[:, idx], "i32").copy()
+    oracle.run_sampled(oracle.Schedule(p, bw, n, k), "i32", cols, coords)
+    assert bits_equal(to_host(x[:, idx], "i32"), cols)
