@@ -341,3 +341,35 @@ def test_more_than_2g_elements_per_rank(o):
     cols = to_host(x0[:, idx], "i32").copy()
     oracle.run_sampled(oracle.Schedule(p, bw, n, k), "i32", cols, coords)
     assert bits_equal(to_host(x[:, idx], "i32"), cols)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+def test_fused_ranges_from_the_middle(o, dtype):
+    """Any slot range [a, b), fused into one launch and started from the
+    state after [0, a) (computed by the oracle), ends in the oracle's state
+    after [0, b): the executor's lanes pick up mid-way state from memory
+    exactly where the earlier slots left it.  One straggler with bubble
+    filling, several stragglers, no straggler, and two server plans (with
+    the local ring fixed at compile time, g = 2, and general, g = 3)."""
+    n = 2048 * 2 + 64 * 7 + 5
+    cases = [("one", 8, _bw(8, {7: 0.875}), None, 8, 6),
+             ("multi", 9, _bw(9, {0: 0.875, 3: 0.75, 8: 0.5}), None, 8, 6),
+             ("ring", 5, _bw(5, {}), None, 8, 6),
+             ("servers g=2", 8, [1.0, 0.5, 1.0, 1.0], (4, 2), 24, 12),
+             ("servers g=3", 9, [1.0, 1.0, 0.75], (3, 3), 24, 12)]
+    for name, p, bw, srv, k, ns in cases:
+        if srv is None:
+            pl, sched = o.optcc_plan(p, bw, n, k), oracle.Schedule(p, bw, n, k)
+        else:
+            pl = o.optcc_plan_servers(srv[0], srv[1], bw, n, k)
+            sched = oracle.Schedule.servers(srv[0], srv[1], bw, n, k)
+        x = rand_inputs(dtype, p, n, 23 + p)
+        for a in range(1, ns):
+            start = oracle.run(sched, dtype, x.copy(), 0, a)
+            for b in range(a + 1, ns + 1):
+                _say(f"case fused range {name} dtype={dtype} [{a},{b})")
+                want = oracle.run(sched, dtype, start.copy(), a, b)
+                d = to_device(start, dtype)
+                o.optcc_allreduce_emulate_slots(d, p, n, dtype, pl, a, b, 1)
+                torch.cuda.synchronize()
+                assert bits_equal(to_host(d, dtype), want), (name, a, b)
