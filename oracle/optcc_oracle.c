@@ -4,8 +4,29 @@
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may include, link,
  * load or call this file.  It shares no code, header, table or constant with
- * the GPU library; both are written independently from the paper and from the
- * readings listed with the design notes.
+ * the GPU library; both are written independently from the paper and from
+ * the same readings of the points the paper leaves open (its pattern figures
+ * are not available):
+ *   - the healthy ring is the healthy ranks in ascending order; section j's
+ *     chain starts at ring[j] and ends at its holder ring[j-1]; Stage 3
+ *     returns the sum to the holder and Stage 4 starts there;
+ *   - in ordering 2 the stragglers' raw values are added at the chain start
+ *     before Stage 1, in straggler order;
+ *   - bubble filling: per segment one point-to-point chunk after the
+ *     sections; the straggler adds its own value first, then ring[0..P'-1];
+ *   - m >= 2, patterns A'/C': the worst straggler finalises as in ordering 1,
+ *     the others add their raw values at the chain start and receive the sum
+ *     after Stage 4 (read literally the printed text is not an AllReduce);
+ *   - one rounding per step; sizes in whole quanta of 64 elements.
+ *
+ * Pins (tests outside this file): exact int32 sums against the definition of
+ * the result; contributor sets (nobody counted twice, everybody counted);
+ * the fp error bound of recursive summation; a chain's association order
+ * against a sequential cumulative sum; flow counts and split sizes against
+ * the paper's worked examples; the lemmas' traffic volumes.  The exact
+ * fp32/bf16 bit patterns follow from the readings above, which the paper
+ * does not fix: parity unpinned by the paper for those bit patterns beyond
+ * the properties listed.
  *
  * Source of every rule below (paper: "Don't Let a Few Network Failures Slow
  * the Entire AllReduce"):
