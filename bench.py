@@ -125,7 +125,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: the OptCC emulation runs the p logical ranks on ONE GPU; "
-              "multi-GPU runs are not part of this build (use --gpus 1).", file=sys.stderr)
+              "it takes --gpus 1 only.", file=sys.stderr)
         sys.exit(2)
 
     import torch

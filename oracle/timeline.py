@@ -14,7 +14,7 @@ Rules (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
 * Sec. 3 correctness (i): a rank transmits only data it already holds: a
   flow waits for the earlier steps of its section that wrote its source's or
   its destination's range.
-* Scheduling policy (this build's reading, the pattern figures being
+* Scheduling policy (a reading of ours, the pattern figures being
   missing): non-preemptive, work-conserving list scheduling in the serial
   step order; at every event time the unstarted flows are scanned in that
   order and each one whose dependencies are done and whose two ports are free
