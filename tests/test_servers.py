@@ -283,3 +283,17 @@ def test_server_graph_capture_replays(o):
             torch.cuda.synchronize()
             assert torch.equal(d.view(iv), eager.view(iv))
         del gr
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("q,g", [(32, 8), (4, 64), (128, 2)])
+def test_server_largest_rank_count(o, q, g):
+    """p = q g = 256 ranks, the executor's limit: 32 servers x 8 GPUs and
+    128 x 2 (local ring fixed at compile time) and 4 servers x 64 GPUs (the
+    general lane, the largest g), bit for bit against the oracle."""
+    from gpu_util import bits_equal
+    slow = {q - 1: 0.5} if q > 4 else {1: 0.875}
+    for dtype in ("i32", "f32"):
+        _say(f"case servers p=256 q={q} g={g} dtype={dtype}")
+        x, ref, got = _run_both(o, q, g, slow, 20000, 24, dtype, seed=q * 7 + g)
+        assert bits_equal(got, ref)
