@@ -34,7 +34,9 @@ extern "C" {
 #define OPTCC_OK 0
 #define OPTCC_EINVAL (-1)      /* bad argument, or arguments that disagree with the plan */
 #define OPTCC_ENOMEM (-2)      /* host or device allocation failed */
-#define OPTCC_EUNSUPPORTED (-3) /* outside the method's domain (p < 3, fewer than 2 healthy ranks) or this library's limits */
+/* outside the method's domain (p < 3, fewer than 2 healthy ranks) or this
+ * library's limits */
+#define OPTCC_EUNSUPPORTED (-3)
 #define OPTCC_EDEVICE (-4)     /* a HIP runtime call failed; the message names it */
 
 #define OPTCC_MAX_RANKS 1024        /* largest p a plan accepts */

@@ -43,7 +43,8 @@ int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
     cut(s.p2p_begin, s.p2p_end, 1);
   }
   DeviceTables d;
-  const size_t sb = pl.segdesc.size() * sizeof(SegDesc), tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
+  const size_t sb = pl.segdesc.size() * sizeof(SegDesc);
+  const size_t tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
   err = hipMalloc(&d.segs, sb);
   if (err == hipSuccess) err = hipMalloc(&d.tiles, tb);
   if (err == hipSuccess) err = hipMemcpy(d.segs, pl.segdesc.data(), sb, hipMemcpyHostToDevice);
@@ -71,7 +72,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     return fail(OPTCC_EINVAL, "unknown dtype");
   if (sb < 0 || se > pl->nslots || sb > se)
     return fail(OPTCC_EINVAL, "slot range must satisfy 0 <= begin <= end <= " + std::to_string(pl->nslots));
-  if (launches != 0 && launches != 1) return fail(OPTCC_EINVAL, "launches must be 0 (one per slot) or 1 (fused)");
+  if (launches != 0 && launches != 1)
+    return fail(OPTCC_EINVAL, "launches must be 0 (one per slot) or 1 (fused)");
   if (p > kMaxRanks) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_EMULATE_RANKS");
   if (N == 0 || sb == se) return OPTCC_OK;  // nothing to move; pointers are not touched
   const size_t es = dtype == OPTCC_BF16 ? 2 : 4;
@@ -81,7 +83,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   for (int r = 0; r < p; ++r) {
     const uintptr_t a = reinterpret_cast<uintptr_t>(bufs[r]);
     if (!a) return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is NULL");
-    if (a % es) return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is not aligned to the element size");
+    if (a % es)
+      return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is not aligned to the element size");
     if (a % 16) vec16 = false;
     ranges.push_back({a, r});
   }

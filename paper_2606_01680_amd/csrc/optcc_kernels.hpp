@@ -388,8 +388,8 @@ __device__ __forceinline__ int local_gpu(int part, int d, int g) {
 // state is straight-line code.  Other ranges, and G = 0, take the general
 // path below (any g, any slot range).
 template <class D, int W, int L, int B, int G>
-__device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, const SegDesc &sd, const int (&j)[L],
-                            const int64_t (&e)[L]) {
+__device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, const SegDesc &sd,
+                                            const int (&j)[L], const int64_t (&e)[L]) {
   using V = Vec<D, W>;
   const int pp = a.pp, g = G > 0 ? G : a.g, part = sd.part;
   const bool t1 = sd.ordering == 1;
@@ -508,130 +508,131 @@ __device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, con
       head_done = true;
     }
   }
-  if (!head_done) {
-  // Slots 2/3 without slot 1 (partial slot ranges only): the leaders already
-  // hold their collected values.
-  if (!i1 && (i2 || i3)) {
+  if (!head_done) {  // general path: any g, any slot range
+    // Slots 2/3 without slot 1 (partial slot ranges only): the leaders already
+    // hold their collected values.
+    if (!i1 && (i2 || i3)) {
 #pragma unroll
-    for (int l = 0; l < L; ++l) v[l] = ld_in<D, W, true>(hr(l, 0, 0), e[l]);
-    if (i2) {
-#pragma unroll
-      for (int l = 0; l < L; ++l) {
-        v[l] = add2<D, W>(ld_in<D, W, true>(sr(0), e[l]), v[l]);
-        st_mid<D, W, true>(hr(l, 0, 0), e[l], v[l]);
-      }
-    }
-    if (i3)
-      for (int t = 1; t < pp; ++t) {
+      for (int l = 0; l < L; ++l) v[l] = ld_in<D, W, true>(hr(l, 0, 0), e[l]);
+      if (i2) {
 #pragma unroll
         for (int l = 0; l < L; ++l) {
-          v[l] = add2<D, W>(ld_in<D, W, true>(hr(l, t, 0), e[l]), v[l]);
-          st_mid<D, W, true>(hr(l, t, 0), e[l], v[l]);
+          v[l] = add2<D, W>(ld_in<D, W, true>(sr(0), e[l]), v[l]);
+          st_mid<D, W, true>(hr(l, 0, 0), e[l], v[l]);
         }
       }
-    have = i3;
-  }
-
-  // The flat input sequence: [0, nA) straggler collect (slot 0), [nA, nA+nB)
-  // chain servers' collects (slot 1, with slots 2/3 folded in at each
-  // leader), then the straggler's operands of slots 4/5.
-  const int nA = i0 ? g : 0, nB = i1 ? pp * g : 0;
-  const int n = nA + nB + (i4 ? 1 : 0) + (i5 ? g - 1 : 0);
-  const int c0 = i4 ? 0 : 1;  // straggler position of the first slot-4/5 operand
-  struct Cur {
-    int i, t, d;  // flat index; chain position and local position inside [nA, nA+nB)
-  };
-  auto cur_ptr = [&](int l, const Cur &c) __attribute__((always_inline)) {
-    if (c.i < nA) return sr(g - 1 - c.i);
-    if (c.i < nA + nB) return hr(l, c.t, c.d);
-    return sr(c.i - nA - nB + c0);
-  };
-  auto cur_next = [&](Cur &c) __attribute__((always_inline)) {
-    if (c.i >= nA && c.i < nA + nB && --c.d < 0) {
-      c.d = g - 1;
-      ++c.t;
-    }
-    ++c.i;
-  };
-  // Every input value feeds one running sum `acc`: the collects (slots 0, 1)
-  // start from the raw value at the far end of a local ring and add one GPU
-  // per step; the straggler's S2 and N2 fold (slots 4, 5) continue from the
-  // holder's partial.  The chain steps (slots 2, 3) run when a leader's
-  // collect completes.
-  auto consume = [&](const Cur &c, const V (&x)[L]) __attribute__((always_inline)) {
-    const bool inA = c.i < nA, inB = !inA && c.i < nA + nB, inC = !inA && !inB;
-    const int d = inA ? g - 1 - c.i : (inB ? c.d : c.i - nA - nB + c0);
-    const bool raw = !inC && d == g - 1;  // the far end of a collect: no step
-    if (inC && c.i == nA + nB) {           // first of slots 4/5: the state it continues
-#pragma unroll
-      for (int l = 0; l < L; ++l) acc[l] = have ? v[l] : ld_in<D, W, true>(d == 0 ? hr(l, pp - 1, 0) : sr(0), e[l]);
-    }
-#pragma unroll
-    for (int l = 0; l < L; ++l) {
-      acc[l] = raw ? x[l] : add2<D, W>(x[l], acc[l]);
-      if (!raw) {
-        void *dst = inB ? hr(l, c.t, d) : sr(d);
-        if (inC && d == g - 1) st_fin<D, W, true>(dst, e[l], acc[l]);  // the global sum
-        else st_mid<D, W, true>(dst, e[l], acc[l]);
-      }
-    }
-    if (inA && d == 0) {  // the straggler leader holds its server's sum
-#pragma unroll
-      for (int l = 0; l < L; ++l) ss[l] = acc[l];
-    }
-    if (inB && d == 0) {  // leader t holds its server's sum
-      if (c.t == 0) {
-        if (i2) {  // slot 2: S3 into the chain start (type 2)
+      if (i3)
+        for (int t = 1; t < pp; ++t) {
 #pragma unroll
           for (int l = 0; l < L; ++l) {
-            const V s2 = i0 ? ss[l] : ld_in<D, W, true>(sr(0), e[l]);
-            v[l] = add2<D, W>(s2, acc[l]);
-            st_mid<D, W, true>(hr(l, 0, 0), e[l], v[l]);
+            v[l] = add2<D, W>(ld_in<D, W, true>(hr(l, t, 0), e[l]), v[l]);
+            st_mid<D, W, true>(hr(l, t, 0), e[l], v[l]);
           }
-        } else {
-#pragma unroll
-          for (int l = 0; l < L; ++l) v[l] = acc[l];
         }
-      } else if (i3) {  // slot 3: S1 hop into leader t
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-          v[l] = add2<D, W>(acc[l], v[l]);
-          st_mid<D, W, true>(hr(l, c.t, 0), e[l], v[l]);
-        }
-      }
-      if (c.t == pp - 1) have = i3;
+      have = i3;
     }
-  };
-  {
-    V buf[B][L];
-    Cur pc{0, 0, g - 1}, cc{0, 0, g - 1};
-#pragma unroll
-    for (int u = 0; u < B; ++u)
-      if (u < n) {
-#pragma unroll
-        for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W, true>(cur_ptr(l, pc), e[l]);
-        cur_next(pc);
+
+    // The flat input sequence: [0, nA) straggler collect (slot 0), [nA, nA+nB)
+    // chain servers' collects (slot 1, with slots 2/3 folded in at each
+    // leader), then the straggler's operands of slots 4/5.
+    const int nA = i0 ? g : 0, nB = i1 ? pp * g : 0;
+    const int n = nA + nB + (i4 ? 1 : 0) + (i5 ? g - 1 : 0);
+    const int c0 = i4 ? 0 : 1;  // straggler position of the first slot-4/5 operand
+    struct Cur {
+      int i, t, d;  // flat index; chain position and local position inside [nA, nA+nB)
+    };
+    auto cur_ptr = [&](int l, const Cur &c) __attribute__((always_inline)) {
+      if (c.i < nA) return sr(g - 1 - c.i);
+      if (c.i < nA + nB) return hr(l, c.t, c.d);
+      return sr(c.i - nA - nB + c0);
+    };
+    auto cur_next = [&](Cur &c) __attribute__((always_inline)) {
+      if (c.i >= nA && c.i < nA + nB && --c.d < 0) {
+        c.d = g - 1;
+        ++c.t;
       }
-    for (int t0 = 0; t0 < n; t0 += B) {
+      ++c.i;
+    };
+    // Every input value feeds one running sum `acc`: the collects (slots 0, 1)
+    // start from the raw value at the far end of a local ring and add one GPU
+    // per step; the straggler's S2 and N2 fold (slots 4, 5) continue from the
+    // holder's partial.  The chain steps (slots 2, 3) run when a leader's
+    // collect completes.
+    auto consume = [&](const Cur &c, const V (&x)[L]) __attribute__((always_inline)) {
+      const bool inA = c.i < nA, inB = !inA && c.i < nA + nB, inC = !inA && !inB;
+      const int d = inA ? g - 1 - c.i : (inB ? c.d : c.i - nA - nB + c0);
+      const bool raw = !inC && d == g - 1;  // the far end of a collect: no step
+      if (inC && c.i == nA + nB) {           // first of slots 4/5: the state it continues
+#pragma unroll
+        for (int l = 0; l < L; ++l)
+          acc[l] = have ? v[l] : ld_in<D, W, true>(d == 0 ? hr(l, pp - 1, 0) : sr(0), e[l]);
+      }
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        acc[l] = raw ? x[l] : add2<D, W>(x[l], acc[l]);
+        if (!raw) {
+          void *dst = inB ? hr(l, c.t, d) : sr(d);
+          if (inC && d == g - 1) st_fin<D, W, true>(dst, e[l], acc[l]);  // the global sum
+          else st_mid<D, W, true>(dst, e[l], acc[l]);
+        }
+      }
+      if (inA && d == 0) {  // the straggler leader holds its server's sum
+#pragma unroll
+        for (int l = 0; l < L; ++l) ss[l] = acc[l];
+      }
+      if (inB && d == 0) {  // leader t holds its server's sum
+        if (c.t == 0) {
+          if (i2) {  // slot 2: S3 into the chain start (type 2)
+#pragma unroll
+            for (int l = 0; l < L; ++l) {
+              const V s2 = i0 ? ss[l] : ld_in<D, W, true>(sr(0), e[l]);
+              v[l] = add2<D, W>(s2, acc[l]);
+              st_mid<D, W, true>(hr(l, 0, 0), e[l], v[l]);
+            }
+          } else {
+#pragma unroll
+            for (int l = 0; l < L; ++l) v[l] = acc[l];
+          }
+        } else if (i3) {  // slot 3: S1 hop into leader t
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            v[l] = add2<D, W>(acc[l], v[l]);
+            st_mid<D, W, true>(hr(l, c.t, 0), e[l], v[l]);
+          }
+        }
+        if (c.t == pp - 1) have = i3;
+      }
+    };
+    {
+      V buf[B][L];
+      Cur pc{0, 0, g - 1}, cc{0, 0, g - 1};
 #pragma unroll
       for (int u = 0; u < B; ++u)
-        if (t0 + u < n) {
-          consume(cc, buf[u]);
-          cur_next(cc);
-          if (t0 + u + B < n) {
+        if (u < n) {
 #pragma unroll
-            for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W, true>(cur_ptr(l, pc), e[l]);
-            cur_next(pc);
-          }
+          for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W, true>(cur_ptr(l, pc), e[l]);
+          cur_next(pc);
         }
+      for (int t0 = 0; t0 < n; t0 += B) {
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+          if (t0 + u < n) {
+            consume(cc, buf[u]);
+            cur_next(cc);
+            if (t0 + u + B < n) {
+#pragma unroll
+              for (int l = 0; l < L; ++l) buf[u][l] = ld_in<D, W, true>(cur_ptr(l, pc), e[l]);
+              cur_next(pc);
+            }
+          }
+      }
+    }
+    if (i4 || i5) {  // slots 4/5 ran: the straggler's running sum is the state
+#pragma unroll
+      for (int l = 0; l < L; ++l) v[l] = acc[l];
+      have = true;
     }
   }
-  if (i4 || i5) {  // slots 4/5 ran: the straggler's running sum is the state
-#pragma unroll
-    for (int l = 0; l < L; ++l) v[l] = acc[l];
-    have = true;
-  }
-  }  // general path
 
   if (t1 && in_range(a, 6)) {  // slot 6: N3, the global sum back to the leader
 #pragma unroll

@@ -84,7 +84,8 @@ void for_each_server_step(const optcc_plan_t &pl, Fn &&fn) {
             break;
           case 1:  // N1 collect onto every healthy leader
             for (int h = 0; h < pp; ++h)
-              for (int d = g - 2; d >= 0; --d) step(1, loc(pl.ring[(size_t)h], d), loc(pl.ring[(size_t)h], d + 1));
+              for (int d = g - 2; d >= 0; --d)
+                step(1, loc(pl.ring[(size_t)h], d), loc(pl.ring[(size_t)h], d + 1));
             break;
           case 2:  // S3 (type 2): straggler's sum into the chain start
             if (!t1) step(1, lead(0), loc(sv, 0));
@@ -302,7 +303,8 @@ extern "C" const char *optcc_last_error(void) { return g_last_error.c_str(); }
 extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_t **out) {
   set_error("");
   if (!out) return fail(OPTCC_EINVAL, "out is NULL");
-  if (p < 3) return fail(OPTCC_EUNSUPPORTED, "p must be >= 3 (the method needs a straggler and two healthy ranks)");
+  if (p < 3)
+    return fail(OPTCC_EUNSUPPORTED, "p must be >= 3 (the method needs a straggler and two healthy ranks)");
   if (p > OPTCC_MAX_RANKS) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_RANKS");
   if (N < 0 || N > ((int64_t)1 << 46)) return fail(OPTCC_EINVAL, "N must be in [0, 2^46]");
   if (k < 4 || k % 4 != 0 || k > (1 << 24))
@@ -328,7 +330,8 @@ extern "C" int optcc_plan(int p, const double *bw, int64_t N, int k, optcc_plan_
       return fail(OPTCC_EUNSUPPORTED, "fewer than 2 healthy ranks: no ring to reduce-scatter on");
     }
     if (pl->m == 0) pl->kind = OPTCC_KIND_RING;
-    else if (pl->m == 1) pl->kind = pl->ell[(size_t)pl->strag[0]] >= 2.0 ? OPTCC_KIND_SINGLE_GE2 : OPTCC_KIND_SINGLE_LT2;
+    else if (pl->m == 1)
+      pl->kind = pl->ell[(size_t)pl->strag[0]] >= 2.0 ? OPTCC_KIND_SINGLE_GE2 : OPTCC_KIND_SINGLE_LT2;
     else pl->kind = OPTCC_KIND_MULTI;
 
     const int64_t nq = (N + kQuantum - 1) / kQuantum;
