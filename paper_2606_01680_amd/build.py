@@ -69,7 +69,22 @@ def build_c_check() -> str:
     return C_CHECK
 
 
+SANITIZE_SRC = os.path.join(ROOT, "tests", "host_sanitize.cpp")
+SANITIZE = os.path.join(ROOT, "tests", "host_sanitize")
+
+
+def build_host_sanitize() -> str:
+    """Compile the host half of the library (optcc_plan.cpp, no device code)
+    with its test driver under AddressSanitizer and UndefinedBehaviorSanitizer."""
+    _run(["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+          "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", f"-I{INCLUDE}", f"-I{CSRC}",
+          SANITIZE_SRC, os.path.join(CSRC, "optcc_plan.cpp"), "-o", SANITIZE + ".tmp"])
+    os.replace(SANITIZE + ".tmp", SANITIZE)
+    return SANITIZE
+
+
 if __name__ == "__main__":
     build()
     build_c_check()
+    build_host_sanitize()
     sys.exit(0)
