@@ -164,3 +164,17 @@ def test_server_validator_uses_nvlink_ports():
     bad = list(good)
     bad[i] = (s, s + 2 * (e - s))  # an NVLink flow at NIC speed
     assert any("duration" in x for x in T.validate(sched, bw, bad))
+
+
+@pytest.mark.parametrize("w", ["q4g4_bf16", "q16g4_f32"])
+def test_server_workload_evaluated_times(o, w):
+    """Full-size server workloads: the evaluated makespan lies above the
+    tight multi-GPU bound (App. B.3) and within 40 % of the App. E closed
+    form (the greedy order does not reproduce the eight-row N-S overlay)."""
+    from paper_2606_01680_amd.workloads import WORKLOADS
+    W = WORKLOADS[w]
+    pl = o.optcc_plan_servers(W.q, W.g, W.bandwidths, W.n, W.k)
+    mk, _, _ = pl.timeline(with_flows=False)
+    lb = o.optcc_lower_bound_servers(W.q, W.g, W.bandwidths, W.n)
+    closed = o.optcc_model_time(pl)
+    assert lb * (1 - 1e-12) <= mk <= 1.4 * closed
