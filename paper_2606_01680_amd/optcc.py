@@ -209,27 +209,46 @@ def optcc_plan_free(plan: Plan) -> None:
         _lib.optcc_plan_free(h)
 
 
-def _ptr_array(bufs, p):
-    """bufs: a [p, N] device tensor or a sequence of p device tensors."""
+ESIZE = {"f32": 4, "bf16": 2, "i32": 4}
+
+
+def _ptr_array(bufs, p, n=None, dtype=None):
+    """bufs: a [p, N] device tensor or a sequence of p device tensors (or raw
+    device addresses).  Tensors must hold N elements per rank of the element
+    size of `dtype`: the library reads and writes N elements at each address
+    and cannot see allocation sizes."""
     try:
         import torch
     except ImportError:  # pragma: no cover
         torch = None
+
+    if dtype is not None and dtype not in ESIZE:
+        raise ValueError(f"unknown dtype {dtype!r}")
+
+    def check(t, what):
+        if dtype is not None and t.element_size() != ESIZE[dtype]:
+            raise ValueError(f"{what} has {t.element_size()}-byte elements, dtype {dtype!r} "
+                             f"needs {ESIZE[dtype]}")
+        if n is not None and t.shape[-1] != n:
+            raise ValueError(f"{what} holds {t.shape[-1]} elements per rank, N is {n}")
+
     if torch is not None and isinstance(bufs, torch.Tensor):
         if bufs.dim() != 2 or bufs.shape[0] != p or not bufs.is_contiguous():
             raise ValueError("bufs must be a contiguous [p, N] tensor")
         if not bufs.is_cuda:
             raise ValueError("bufs must live on the GPU")
+        check(bufs, "bufs")
         base, stride = bufs.data_ptr(), bufs.stride(0) * bufs.element_size()
         ptrs = [base + r * stride for r in range(p)]
     else:
         if len(bufs) != p:
             raise ValueError("need p buffers")
         ptrs = []
-        for b in bufs:
+        for r, b in enumerate(bufs):
             if torch is not None and isinstance(b, torch.Tensor):
-                if not b.is_cuda or not b.is_contiguous():
-                    raise ValueError("every buffer must be a contiguous GPU tensor")
+                if not b.is_cuda or not b.is_contiguous() or b.dim() != 1:
+                    raise ValueError("every buffer must be a contiguous 1-D GPU tensor")
+                check(b, f"bufs[{r}]")
                 ptrs.append(b.data_ptr())
             else:
                 ptrs.append(int(b))
@@ -246,14 +265,14 @@ def _stream(stream):
 def optcc_allreduce_emulate(bufs, p: int, N: int, dtype: str, plan: Plan, stream=None) -> None:
     """Run the whole schedule in place (one fused launch) on `stream`
     (default: torch's current stream)."""
-    arr = _ptr_array(bufs, p)
+    arr = _ptr_array(bufs, p, int(N), dtype)
     _check(_lib.optcc_allreduce_emulate(arr, int(p), int(N), DTYPES[dtype], plan.handle,
                                         ctypes.c_void_p(_stream(stream))))
 
 
 def optcc_allreduce_emulate_slots(bufs, p: int, N: int, dtype: str, plan: Plan, slot_begin: int,
                                   slot_end: int, launches: int = 1, stream=None) -> None:
-    arr = _ptr_array(bufs, p)
+    arr = _ptr_array(bufs, p, int(N), dtype)
     _check(_lib.optcc_allreduce_emulate_slots(arr, int(p), int(N), DTYPES[dtype], plan.handle,
                                               int(slot_begin), int(slot_end), int(launches),
                                               ctypes.c_void_p(_stream(stream))))

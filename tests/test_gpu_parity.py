@@ -373,3 +373,23 @@ def test_fused_ranges_from_the_middle(o, dtype):
                 o.optcc_allreduce_emulate_slots(d, p, n, dtype, pl, a, b, 1)
                 torch.cuda.synchronize()
                 assert bits_equal(to_host(d, dtype), want), (name, a, b)
+
+
+def test_binding_rejects_mismatched_tensors(o):
+    """The binding refuses tensors whose element size or length disagrees
+    with dtype and N before any pointer reaches the library: the library
+    reads and writes N elements of dtype at every rank address and cannot
+    see allocation sizes."""
+    p, n, k = 5, 1000, 8
+    pl = o.optcc_plan(p, [1, 1, 0.5, 1, 1], n, k)
+    bf = torch.zeros((p, n), dtype=torch.bfloat16, device="cuda:0")
+    with pytest.raises(ValueError, match="element"):
+        o.optcc_allreduce_emulate(bf, p, n, "f32", pl)
+    with pytest.raises(ValueError, match="element"):
+        o.optcc_allreduce_emulate([bf[r] for r in range(p)], p, n, "i32", pl)
+    short = [torch.zeros(n - 1, device="cuda:0") for _ in range(p)]
+    with pytest.raises(ValueError, match="elements per rank"):
+        o.optcc_allreduce_emulate(short, p, n, "f32", pl)
+    with pytest.raises(ValueError, match="dtype"):
+        o.optcc_allreduce_emulate(torch.zeros((p, n), device="cuda:0"), p, n, "f64", pl)
+    torch.cuda.synchronize()
