@@ -1,5 +1,5 @@
 // Device code of the OptCC executor: element types, per-lane step
-// sequences and the kernel.  Included by optcc_exec.hip only.
+// sequences and the kernel.  Included through optcc_launch.hpp.
 //
 // The p logical ranks are p buffers in HBM.  One workgroup takes one tile of
 // 2048 consecutive elements of one segment's ring sections (or of its
@@ -19,6 +19,8 @@
 //   3 Stage 3: the global sum returns to the holder; P2P down
 //   4 Stage 4 allgather holder -> R[j] -> ... -> R[j+P'-2]
 //   5 the global sum reaches the stragglers that did not finalise
+// Plans with several GPUs per server (App. E) run twelve slots, the NVLink
+// phases N1-N4 around the four NIC stages; see server_lane below.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -51,7 +53,8 @@ constexpr int kHopWindow = 16;  // hop loads in flight per vector along a chain
 constexpr bool kNtLoads = OPTCC_NT_LOADS;
 constexpr bool kNtFinal = OPTCC_NT_FINAL;
 constexpr bool kNtMid = OPTCC_NT_MID;
-// fp32/int32 plans with at most this many healthy ranks run two 16-byte
+// fp32/int32 plans whose lanes read at most this many inputs (the healthy
+// ranks with one GPU per server, all p ranks with several) run two 16-byte
 // vectors per lane in lockstep (measured faster for short chains)
 constexpr int kTwoVectorMaxHealthy = 32;
 
