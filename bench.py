@@ -22,7 +22,9 @@ PEAK_GBPS = 8000.0  # MI355X HBM3E
 # device code of the executor (kernels, table layouts, launch choices)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01680_amd", "csrc", f)
                for f in ("optcc_kernels.hpp", "optcc_internal.hpp", "optcc_launch.hpp",
-                         "optcc_exec.hip")]
+                         "optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip",
+                         "optcc_kern_i32.hip", "optcc_kern_f32_g58.hip",
+                         "optcc_kern_bf16_g58.hip", "optcc_kern_i32_g58.hip")]
 
 
 def _code_only(text: str) -> str:

@@ -22,7 +22,8 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
-KERNEL_TUS = ("optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip", "optcc_kern_i32.hip")
+KERNEL_TUS = ("optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip", "optcc_kern_i32.hip",
+              "optcc_kern_f32_g58.hip", "optcc_kern_bf16_g58.hip", "optcc_kern_i32_g58.hip")
 
 
 def sources():

@@ -12,14 +12,20 @@
 namespace optcc {
 namespace kern {
 
+// G = 0 covers element-aligned buffers (one element per access) too;
+// G > 0 expects 16-byte-aligned buffers (vec16).
 template <class D, bool S, int G>
 hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   constexpr int W16 = 16 / (int)sizeof(typename D::S);
   const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
-  if (!vec16) {  // element-aligned buffers: the general lane, one element per access
-    hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, 0, st, a);
-    return hipGetLastError();
+  if constexpr (G == 0) {
+    if (!vec16) {  // element-aligned buffers: one element per access
+      hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
+  } else if (!vec16) {
+    return hipErrorInvalidValue;
   }
   if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
     if (two) {
@@ -31,26 +37,27 @@ hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Several GPUs per server: the usual server sizes g = 2, 4, 8 get a kernel
-// with the local ring fixed at compile time.
-template <class D>
-hipError_t launch_plan(const KArgs &a, bool servers, bool vec16, bool two, hipStream_t st) {
-  if (!servers) return launch<D, false, 0>(a, vec16, two, st);
-  switch (a.g) {
-    case 2: return launch<D, true, 2>(a, vec16, two, st);
-    case 4: return launch<D, true, 4>(a, vec16, two, st);
-    case 8: return launch<D, true, 8>(a, vec16, two, st);
-    default: return launch<D, true, 0>(a, vec16, two, st);
-  }
+// Several GPUs per server, 16-byte path: the kernel with the local ring
+// fixed at compile time when g is one of Gs (else hipErrorInvalidValue).
+template <class D, int... Gs>
+hipError_t launch_fixed_g(const KArgs &a, bool two, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  (void)((a.g == Gs ? (err = launch<D, true, Gs>(a, true, two, st), true) : false) || ...);
+  return err;
 }
 
 }  // namespace kern
 
-// One element type each (optcc_kern_f32.hip, optcc_kern_bf16.hip,
-// optcc_kern_i32.hip): servers selects the several-GPUs-per-server lane,
-// vec16 the 16-byte path, two the two-vectors-per-lane variant.
+// One element type each (optcc_kern_<type>.hip: one GPU per server, and
+// servers of 2-4 GPUs or any other size; optcc_kern_<type>_g58.hip: servers
+// of 5-8 GPUs, split off so that the files compile in parallel): servers
+// selects the several-GPUs-per-server lane, vec16 the 16-byte path, two the
+// two-vectors-per-lane variant.
 hipError_t launch_f32(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
 hipError_t launch_bf16(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
 hipError_t launch_i32(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
+hipError_t launch_f32_g58(const kern::KArgs &a, bool two, hipStream_t st);
+hipError_t launch_bf16_g58(const kern::KArgs &a, bool two, hipStream_t st);
+hipError_t launch_i32_g58(const kern::KArgs &a, bool two, hipStream_t st);
 
 }  // namespace optcc

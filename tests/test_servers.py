@@ -141,8 +141,10 @@ def _run_both(o, q, g, slow, n, k, dtype, seed, slot_end=12, launches=1, kind="n
     return x, ref, to_host(d, dtype)
 
 
+# every server size with a compile-time local ring (2..8) and the general lane (12)
 GPU_PROFILES = [(3, 2, {2: 0.5}), (4, 4, {1: 0.875}), (5, 3, {0: 0.5}), (3, 8, {2: 0.25}),
-                (6, 5, {2: 0.75}), (16, 4, {15: 0.5}), (9, 3, {4: 0.875})]
+                (6, 5, {2: 0.75}), (16, 4, {15: 0.5}), (9, 3, {4: 0.875}), (4, 6, {0: 0.5}),
+                (3, 7, {1: 0.875}), (3, 12, {2: 0.5})]
 GPU_SIZES = [(1, 24), (37, 24), (2048 * 3 + 64 * 5 + 3, 24), (40000, 32)]
 
 
