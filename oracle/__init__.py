@@ -29,8 +29,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "optcc_oracle.c")
 _LIB = os.path.join(_HERE, "liboptcc_oracle.so")
 
-DTYPES = {"f32": 0, "bf16": 1, "i32": 2}
-NP_DTYPES = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32}
+DTYPES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3}
+NP_DTYPES = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "f16": np.uint16}
 KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi", 4: "servers"}
 COPY, REDUCE = 0, 1
 NUM_SLOTS = 6           # one GPU per server
@@ -69,6 +69,8 @@ def lib():
         L.orc_run_sampled.restype = i32
         L.orc_last_error.restype = ctypes.c_char_p
         L.orc_bf16_round_array.argtypes = [vp, vp, i64]
+        L.orc_f16_round_array.argtypes = [vp, vp, i64]
+        L.orc_f16_widen_array.argtypes = [vp, vp, i64]
         _lib = L
     return _lib
 
@@ -199,29 +201,53 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def f16_round(x: np.ndarray) -> np.ndarray:
+    """fp32 -> IEEE binary16 bits, round to nearest even, through the oracle's C rule."""
+    flat = np.ascontiguousarray(x, dtype=np.float32).ravel()
+    out = np.empty(flat.size, np.uint16)
+    lib().orc_f16_round_array(_ptr(flat), _ptr(out), flat.size)
+    return out.reshape(np.shape(x))
+
+
+def f16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """binary16 bits -> values, through the oracle's exact C widening."""
+    flat = np.ascontiguousarray(bits, dtype=np.uint16).ravel()
+    out = np.empty(flat.size, np.float32)
+    lib().orc_f16_widen_array(_ptr(flat), _ptr(out), flat.size)
+    return out.reshape(np.shape(bits)).astype(np.float64)
+
+
+def values_f64(dtype: str, bufs: np.ndarray) -> np.ndarray:
+    """The values a buffer of `dtype` holds, in fp64."""
+    if dtype == "f32":
+        return bufs.astype(np.float64)
+    if dtype == "bf16":
+        return bf16_to_f64(bufs)
+    if dtype == "f16":
+        return f16_to_f64(bufs)
+    raise ValueError("integers are compared exactly")
+
+
 def brute_sum(dtype: str, bufs: np.ndarray) -> np.ndarray:
     """The definition of the result: sum over ranks of every coordinate.
     fp64 for floating point; int32 wraps modulo 2**32 like two's complement."""
-    if dtype == "f32":
-        return bufs.astype(np.float64).sum(axis=0)
-    if dtype == "bf16":
-        return bf16_to_f64(bufs).sum(axis=0)
+    if dtype in ("f32", "bf16", "f16"):
+        return values_f64(dtype, bufs).sum(axis=0)
     s = bufs.astype(np.int64).sum(axis=0)
     return ((s + 2**31) % 2**32 - 2**31).astype(np.int32)
 
 
 def abs_sum(dtype: str, bufs: np.ndarray) -> np.ndarray:
-    if dtype == "f32":
-        return np.abs(bufs.astype(np.float64)).sum(axis=0)
-    if dtype == "bf16":
-        return np.abs(bf16_to_f64(bufs)).sum(axis=0)
-    raise ValueError("no tolerance for integers: they are exact")
+    if dtype == "i32":
+        raise ValueError("no tolerance for integers: they are exact")
+    return np.abs(values_f64(dtype, bufs)).sum(axis=0)
 
 
 def tolerance(dtype: str, p: int, bufs: np.ndarray) -> np.ndarray:
-    """Elementwise bound |y - sum| <= p u sum|x_i| with u = 2**-24 (fp32) or
-    2**-8 (bf16); it covers recursive summation with one rounding per add."""
-    u = 2.0 ** -24 if dtype == "f32" else 2.0 ** -8
+    """Elementwise bound |y - sum| <= p u sum|x_i| with u = 2**-24 (fp32),
+    2**-11 (fp16) or 2**-8 (bf16); it covers recursive summation with one
+    rounding per add (no overflow)."""
+    u = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}[dtype]
     return p * u * abs_sum(dtype, bufs)
 
 

@@ -51,8 +51,10 @@
  *            listed order; dst <- narrow(acc)
  * widen/narrow are the identity for fp32 and int32 (int32 adds wrap modulo
  * 2^32); for bf16, widen is the exact 16-bit shift to fp32 and narrow rounds
- * fp32 to bf16 to nearest, ties to even.  Every step rounds once, so a chain
- * of hops rounds at every hop, as a bf16 wire would.
+ * fp32 to bf16 to nearest, ties to even; for fp16 (IEEE 754 binary16) widen
+ * is exact and narrow rounds to nearest, ties to even, with subnormals kept
+ * and overflow to infinity.  Every step rounds once, so a chain of hops
+ * rounds at every hop, as a 16-bit wire would.
  *
  * Steps carry a slot number 0..5 that orders the stages of every section:
  *   0 straggler raw values folded into the chain start (ordering 2's Stage 3,
@@ -92,6 +94,7 @@
 #define ORC_F32 0
 #define ORC_BF16 1
 #define ORC_I32 2
+#define ORC_F16 3
 
 #define ORC_COPY 0
 #define ORC_REDUCE 1
@@ -567,7 +570,64 @@ static uint16_t bf16_narrow(float f) {
   return (uint16_t)(u >> 16);
 }
 
+/* binary16 -> fp32, exact.  Layout: sign, 5-bit exponent (bias 15), 10-bit
+ * fraction; exponent 0 holds zeros and subnormals (fraction * 2^-24), 31
+ * infinities and NaNs (returned quiet, payload kept). */
+static float f16_widen(uint16_t h) {
+  const uint32_t sign = (uint32_t)(h & 0x8000u) << 16;
+  const uint32_t e = (h >> 10) & 0x1fu, m = h & 0x3ffu;
+  uint32_t u;
+  if (e == 0) {
+    float f = ldexpf((float)m, -24);  /* exact: m < 2^10 */
+    memcpy(&u, &f, 4);
+    u |= sign;
+  } else if (e == 31) {
+    u = sign | 0x7f800000u | (m ? 0x00400000u | (m << 13) : 0u);
+  } else {
+    u = sign | ((e - 15u + 127u) << 23) | (m << 13);
+  }
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* fp32 -> binary16, round to nearest, ties to even.  |f| >= 65520 (the
+ * midpoint between the largest finite value 65504 and 2^16) becomes
+ * infinity; values below 2^-14 become subnormals (units of 2^-24), and
+ * |f| <= 2^-25 (a tie with zero at most) becomes zero. */
+static uint16_t f16_narrow(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  const uint16_t sign = (uint16_t)((u >> 16) & 0x8000u);
+  const uint32_t a = u & 0x7fffffffu;
+  if (a > 0x7f800000u) return (uint16_t)(sign | 0x7e00u | ((a >> 13) & 0x3ffu));  /* NaN */
+  if (a >= 0x477ff000u) return (uint16_t)(sign | 0x7c00u);  /* >= 65520: infinity */
+  if (a >= 0x38800000u) {  /* normal result: keep 10 of the 23 fraction bits */
+    const uint32_t e = (a >> 23) - 127u + 15u;
+    uint32_t h = (e << 10) | ((a >> 13) & 0x3ffu);
+    const uint32_t rem = a & 0x1fffu;
+    if (rem > 0x1000u || (rem == 0x1000u && (h & 1u))) h += 1u;  /* may carry into e */
+    return (uint16_t)(sign | h);
+  }
+  if (a <= 0x33000000u) return sign;  /* |f| <= 2^-25 */
+  /* subnormal result: m = |f| / 2^-24 rounded; |f| = mm * 2^(e - 150) */
+  const uint32_t e = a >> 23, mm = (a & 0x7fffffu) | 0x800000u;
+  const uint32_t sh = 126u - e;  /* 14 .. 24 */
+  uint32_t m = mm >> sh;
+  const uint32_t rem = mm & ((1u << sh) - 1u), half = 1u << (sh - 1u);
+  if (rem > half || (rem == half && (m & 1u))) m += 1u;
+  return (uint16_t)(sign | m);
+}
+
 uint16_t orc_bf16_round(float f) { return bf16_narrow(f); }
+
+void orc_f16_round_array(const float *x, uint16_t *y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) y[i] = f16_narrow(x[i]);
+}
+
+void orc_f16_widen_array(const uint16_t *x, float *y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) y[i] = f16_widen(x[i]);
+}
 
 void orc_bf16_round_array(const float *x, uint16_t *y, int64_t n) {
   for (int64_t i = 0; i < n; ++i) y[i] = bf16_narrow(x[i]);
@@ -588,6 +648,12 @@ static void apply_elem(int dtype, const orc_step *st, const int32_t *srcs, void 
     float acc = bf16_widen(b[st->dst][c]);
     for (int i = 0; i < st->nsrc; ++i) acc = acc + bf16_widen(b[srcs[i]][c]);
     b[st->dst][c] = bf16_narrow(acc);
+  } else if (dtype == ORC_F16) {
+    uint16_t **b = (uint16_t **)bufs;
+    if (st->op == ORC_COPY) { b[st->dst][c] = b[srcs[0]][c]; return; }
+    float acc = f16_widen(b[st->dst][c]);
+    for (int i = 0; i < st->nsrc; ++i) acc = acc + f16_widen(b[srcs[i]][c]);
+    b[st->dst][c] = f16_narrow(acc);
   } else {
     uint32_t **b = (uint32_t **)bufs;
     if (st->op == ORC_COPY) { b[st->dst][c] = b[srcs[0]][c]; return; }
@@ -600,7 +666,7 @@ static void apply_elem(int dtype, const orc_step *st, const int32_t *srcs, void 
 /* Execute every step with slot in [slot_lo, slot_hi), serially, in order,
  * over whole rank buffers (p host pointers of N elements). */
 int orc_run(const orc_sched *s, int dtype, void **bufs, int slot_lo, int slot_hi) {
-  if (dtype < 0 || dtype > 2) { g_err = "bad dtype"; return -1; }
+  if (dtype < 0 || dtype > 3) { g_err = "bad dtype"; return -1; }
   for (int64_t i = 0; i < s->nsteps; ++i) {
     const orc_step *st = &s->steps[i];
     if (st->slot < slot_lo || st->slot >= slot_hi) continue;
@@ -615,7 +681,7 @@ int orc_run(const orc_sched *s, int dtype, void **bufs, int slot_lo, int slot_hi
  * coords[i]).  Used to check full-size runs at sampled coordinates. */
 int orc_run_sampled(const orc_sched *s, int dtype, void **cols, const int64_t *coords,
                     int64_t S, int slot_lo, int slot_hi) {
-  if (dtype < 0 || dtype > 2) { g_err = "bad dtype"; return -1; }
+  if (dtype < 0 || dtype > 3) { g_err = "bad dtype"; return -1; }
   for (int64_t i = 1; i < S; ++i)
     if (coords[i] <= coords[i - 1]) { g_err = "coords must be strictly increasing"; return -1; }
   for (int64_t i = 0; i < s->nsteps; ++i) {

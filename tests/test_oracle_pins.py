@@ -34,6 +34,8 @@ def _rand(dtype, p, n, seed):
     x = rng.standard_normal((p, n)).astype(np.float32)
     if dtype == "bf16":
         return oracle.bf16_round(x)
+    if dtype == "f16":
+        return oracle.f16_round(x)
     return x
 
 
@@ -125,16 +127,17 @@ def test_int32_exact_and_provenance(orc, p, slow, n, k):
 
 
 @pytest.mark.parametrize("p,slow", CASES)
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 def test_float_error_bound(orc, p, slow, dtype):
     """Sec. 3 result within the recursive-summation bound p u sum|x_i|
-    (u = 2^-24 fp32, 2^-8 bf16), and every rank's buffer bitwise identical."""
+    (u = 2^-24 fp32, 2^-11 fp16, 2^-8 bf16), and every rank's buffer bitwise
+    identical."""
     n, k = 64 * 37 + 5, 8
     s = orc.Schedule(p, _bw(p, slow), n, k)
     x = _rand(dtype, p, n, 11 * p)
     y = orc.run(s, dtype, x.copy())
     assert (y == y[0][None, :]).all()
-    got = y[0].astype(np.float64) if dtype == "f32" else orc.bf16_to_f64(y[0])
+    got = orc.values_f64(dtype, y[0])
     err = np.abs(got - orc.brute_sum(dtype, x))
     assert (err <= orc.tolerance(dtype, p, x)).all()
 
@@ -154,6 +157,38 @@ def test_bf16_rounding_matches_library():
     ours = oracle.bf16_round(x[keep])
     ref = torch.from_numpy(x[keep].copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert (ours == ref).all()
+
+
+def test_f16_conversions_match_library():
+    """fp16 narrowing is IEEE binary16 round-to-nearest-even with subnormals
+    and overflow to infinity, widening is exact: torch's CPU conversions are
+    library routines of the same definitions.  All 2^16 half patterns widen
+    identically (NaN payloads aside) and narrow back to themselves; 2^20
+    random fp32 patterns plus the boundaries (largest finite, the overflow
+    midpoint 65520, the smallest normal and subnormal, the 2^-25 tie, signed
+    zeros, infinities) narrow identically."""
+    import torch
+    h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ours = oracle.f16_to_f64(h)
+    ref = torch.from_numpy(h.view(np.int16).copy()).view(torch.float16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert (np.isnan(ours) == nan).all()
+    assert (ours[~nan] == ref[~nan]).all()
+    assert (np.signbit(ours[~nan]) == np.signbit(ref[~nan])).all()
+    assert (oracle.f16_round(ours[~nan].astype(np.float32)) == h[~nan]).all()
+    rng = np.random.default_rng(4)
+    bits = rng.integers(0, 2**32, size=1 << 20, dtype=np.uint64).astype(np.uint32)
+    # values from 2^-30 to 2^20 hit the subnormal, normal and overflow paths often
+    near = (rng.integers(97, 148, size=1 << 18).astype(np.uint32) << 23) | \
+        rng.integers(0, 1 << 23, size=1 << 18).astype(np.uint32)
+    edge = np.array([0x477fe000, 0x477ff000, 0x477fefff, 0x477ff001, 0x38800000, 0x387fffff,
+                     0x33800000, 0x33000000, 0x33000001, 0x32ffffff, 0x00000000, 0x80000000,
+                     0x7f800000, 0xff800000, 0x3f800000, 0x3f801000, 0x3f803000, 0x3f800fff],
+                    np.uint32)
+    x = np.concatenate([bits, near, near | 0x80000000, edge]).view(np.float32)
+    x = x[~np.isnan(x)]
+    ref = torch.from_numpy(x.copy()).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
+    assert (oracle.f16_round(x) == ref).all()
 
 
 def test_fp32_association_is_the_chain(orc):
@@ -413,14 +448,14 @@ def test_servers_int32_exact_and_provenance(orc, q, g, slow, n):
 
 
 @pytest.mark.parametrize("q,g,slow", SERVER_CASES)
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 def test_servers_float_error_bound(orc, q, g, slow, dtype):
     n = 64 * 40 + 3
     s = orc.Schedule.servers(q, g, _sbw(q, slow), n, 24)
     x = _rand(dtype, s.p, n, 5 * q + g)
     y = orc.run(s, dtype, x.copy())
     assert (y == y[0][None, :]).all()
-    got = y[0].astype(np.float64) if dtype == "f32" else orc.bf16_to_f64(y[0])
+    got = orc.values_f64(dtype, y[0])
     assert (np.abs(got - orc.brute_sum(dtype, x)) <= orc.tolerance(dtype, s.p, x)).all()
 
 
