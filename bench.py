@@ -23,8 +23,9 @@ PEAK_GBPS = 8000.0  # MI355X HBM3E
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01680_amd", "csrc", f)
                for f in ("optcc_kernels.hpp", "optcc_internal.hpp", "optcc_launch.hpp",
                          "optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip",
-                         "optcc_kern_i32.hip", "optcc_kern_f32_g58.hip",
-                         "optcc_kern_bf16_g58.hip", "optcc_kern_i32_g58.hip")]
+                         "optcc_kern_i32.hip", "optcc_kern_f16.hip",
+                         "optcc_kern_f32_g58.hip", "optcc_kern_bf16_g58.hip",
+                         "optcc_kern_i32_g58.hip", "optcc_kern_f16_g58.hip")]
 
 
 def _code_only(text: str) -> str:
@@ -91,7 +92,7 @@ def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
         if host is None or host.shape[1] < end:
             host = np.empty((w.p, w.n), dtype=oracle.NP_DTYPES[w.dtype])
         src = x0[:, :end].cpu()
-        if w.dtype == "bf16":
+        if w.dtype in ("bf16", "f16"):
             import torch
             host[:, :end] = src.view(torch.int16).numpy().view(np.uint16)
         else:
@@ -208,7 +209,7 @@ def main():
         x.copy_(x0)
         step()
         torch.cuda.synchronize()
-        iv = x.view(torch.int16) if w.dtype == "bf16" else x.view(torch.int32)
+        iv = x.view(torch.int16) if x.element_size() == 2 else x.view(torch.int32)
         ok = all(torch.equal(iv[r], iv[0]) for r in range(1, w.p))
         chunk = max(1 << 16, (1 << 28) // w.p)
         for c0 in range(0, w.n, chunk):
@@ -218,7 +219,7 @@ def main():
                 ok &= torch.equal(x[0, c0:c1], ((want + 2**31) % 2**32 - 2**31).to(torch.int32))
             else:
                 xs = x0[:, c0:c1].to(torch.float64)
-                u = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8
+                u = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}[w.dtype]
                 err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
                 ok &= bool((err <= w.p * u * xs.abs().sum(0)).all())
         check = "pass" if ok else "FAIL"

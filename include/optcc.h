@@ -48,7 +48,7 @@ extern "C" {
 
 typedef struct optcc_plan optcc_plan_t;
 
-typedef enum { OPTCC_F32 = 0, OPTCC_BF16 = 1, OPTCC_I32 = 2 } optcc_dtype_t;
+typedef enum { OPTCC_F32 = 0, OPTCC_BF16 = 1, OPTCC_I32 = 2, OPTCC_F16 = 3 } optcc_dtype_t;
 
 typedef enum {
   OPTCC_KIND_RING = 0,       /* no straggler: the ring of Sec. 3 (T0) */
@@ -130,8 +130,10 @@ void optcc_plan_free(optcc_plan_t *plan);
  *          of `dtype`, aligned to the element size.  Buffers must not overlap.
  *          16-byte alignment of every pointer enables the vector path.
  *   p, N   must equal the plan's
- *   dtype  OPTCC_F32 (fp32 adds), OPTCC_BF16 (fp32 accumulation, one
- *          round-to-nearest-even per step), OPTCC_I32 (adds modulo 2^32)
+ *   dtype  OPTCC_F32 (fp32 adds), OPTCC_BF16 and OPTCC_F16 (IEEE binary16)
+ *          (fp32 accumulation, one round-to-nearest-even per step; fp16
+ *          keeps subnormals and overflows to infinity), OPTCC_I32 (adds
+ *          modulo 2^32)
  *
  * Every step writes its destination rank's buffer; a partial sum that the
  * next step of the same section consumes is kept in registers.  The result is

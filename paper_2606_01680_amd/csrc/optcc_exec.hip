@@ -68,7 +68,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
   if (!bufs) return fail(OPTCC_EINVAL, "bufs is NULL");
   if (p != pl->p || N != pl->n) return fail(OPTCC_EINVAL, "p or N differ from the plan's");
-  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
+  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32 && dtype != OPTCC_F16)
     return fail(OPTCC_EINVAL, "unknown dtype");
   if (sb < 0 || se > pl->nslots || sb > se)
     return fail(OPTCC_EINVAL, "slot range must satisfy 0 <= begin <= end <= " + std::to_string(pl->nslots));
@@ -76,7 +76,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     return fail(OPTCC_EINVAL, "launches must be 0 (one per slot) or 1 (fused)");
   if (p > kMaxRanks) return fail(OPTCC_EUNSUPPORTED, "p exceeds OPTCC_MAX_EMULATE_RANKS");
   if (N == 0 || sb == se) return OPTCC_OK;  // nothing to move; pointers are not touched
-  const size_t es = dtype == OPTCC_BF16 ? 2 : 4;
+  const size_t es = dtype == OPTCC_BF16 || dtype == OPTCC_F16 ? 2 : 4;
   // pointers: non-NULL, element-aligned, pairwise disjoint
   std::vector<std::pair<uintptr_t, int>> ranges;
   bool vec16 = true;
@@ -130,6 +130,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     switch (dtype) {
       case OPTCC_F32: err = launch_f32(a, servers, vec16, two, st); break;
       case OPTCC_BF16: err = launch_bf16(a, servers, vec16, false, st); break;
+      case OPTCC_F16: err = launch_f16(a, servers, vec16, false, st); break;
       default: err = launch_i32(a, servers, vec16, two, st); break;
     }
     if (err != hipSuccess)

@@ -101,6 +101,16 @@ struct BF16 {
   }
 };
 
+// IEEE binary16: widening is exact (v_cvt_f32_f16); narrowing rounds to
+// nearest even in the default rounding mode, keeps subnormals (fp16
+// denormals are not flushed) and overflows to infinity (v_cvt_f16_f32).
+struct F16 {
+  using S = uint16_t;
+  using A = float;
+  __device__ static A widen(S x) { return (float)__builtin_bit_cast(_Float16, x); }
+  __device__ static S narrow(A f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+};
+
 template <class D, int W>
 struct alignas(sizeof(typename D::S) * W) Vec {
   typename D::S v[W];

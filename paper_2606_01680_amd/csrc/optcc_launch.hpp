@@ -1,6 +1,6 @@
 // Kernel launches of the OptCC executor: the kernel variants of one element
 // type and the choice among them.  Each optcc_kern_*.hip instantiates one
-// element type; optcc_exec.hip calls them through launch_f32/bf16/i32.
+// element type; optcc_exec.hip calls them through launch_f32/bf16/i32/f16.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -56,8 +56,10 @@ hipError_t launch_fixed_g(const KArgs &a, bool two, hipStream_t st) {
 hipError_t launch_f32(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
 hipError_t launch_bf16(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
 hipError_t launch_i32(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
+hipError_t launch_f16(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st);
 hipError_t launch_f32_g58(const kern::KArgs &a, bool two, hipStream_t st);
 hipError_t launch_bf16_g58(const kern::KArgs &a, bool two, hipStream_t st);
 hipError_t launch_i32_g58(const kern::KArgs &a, bool two, hipStream_t st);
+hipError_t launch_f16_g58(const kern::KArgs &a, bool two, hipStream_t st);
 
 }  // namespace optcc

@@ -632,11 +632,11 @@ extern "C" double optcc_lower_bound_servers(int q, int g, const double *bw, int6
 extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, int sb, int se,
                                   int launches, int64_t *rd, int64_t *wr) {
   if (!pl || !rd || !wr) return fail(OPTCC_EINVAL, "NULL argument");
-  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32)
+  if (dtype != OPTCC_F32 && dtype != OPTCC_BF16 && dtype != OPTCC_I32 && dtype != OPTCC_F16)
     return fail(OPTCC_EINVAL, "unknown dtype");
   if (sb < 0 || se > pl->nslots || sb > se) return fail(OPTCC_EINVAL, "bad slot range");
   if (launches != 0 && launches != 1) return fail(OPTCC_EINVAL, "launches must be 0 or 1");
-  const int64_t es = dtype == OPTCC_BF16 ? 2 : 4;
+  const int64_t es = dtype == OPTCC_BF16 || dtype == OPTCC_F16 ? 2 : 4;
   int64_t r = 0, w = 0;
   auto lane = [&](int ord, bool p2p, int b, int e, int64_t *l, int64_t *s) {
     if (pl->kind == OPTCC_KIND_SERVERS) server_lane_traffic(*pl, ord, b, e, l, s);

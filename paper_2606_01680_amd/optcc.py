@@ -21,7 +21,7 @@ OPTCC_NUM_SERVER_SLOTS = 12
 OPTCC_MAX_GPUS_PER_SERVER = 64
 OPTCC_QUANTUM = 64
 OPTCC_MAX_EMULATE_RANKS = 256
-DTYPES = {"f32": 0, "bf16": 1, "i32": 2}
+DTYPES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3}
 KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi", 4: "servers"}
 
 EXPORTED = ("optcc_plan", "optcc_plan_servers", "optcc_plan_free", "optcc_allreduce_emulate",
@@ -209,7 +209,7 @@ def optcc_plan_free(plan: Plan) -> None:
         _lib.optcc_plan_free(h)
 
 
-ESIZE = {"f32": 4, "bf16": 2, "i32": 4}
+ESIZE = {"f32": 4, "bf16": 2, "i32": 4, "f16": 2}
 
 
 def _ptr_array(bufs, p, n=None, dtype=None):

@@ -14,8 +14,9 @@ from dataclasses import dataclass, field
 
 import torch
 
-TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32}
-ESIZE = {"f32": 4, "bf16": 2, "i32": 4}
+TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32,
+                "f16": torch.float16}
+ESIZE = {"f32": 4, "bf16": 2, "i32": 4, "f16": 2}
 
 
 @dataclass(frozen=True)
@@ -52,6 +53,9 @@ WORKLOADS = {
                        "int32 run of the p=8 workload"),
     "p16_bf16": Workload("p16_bf16", 2, 16, _bw(16, {15: 0.5}), 1 << 26, 128, "bf16",
                          "normal_1e-2", "rank 15 at 50% bandwidth"),
+    # the p = 16 workload with IEEE fp16 gradients (loss-scaled mixed precision)
+    "p16_f16": Workload("p16_f16", 8, 16, _bw(16, {15: 0.5}), 1 << 26, 128, "f16",
+                        "normal_1e-2", "fp16 run of the p=16 workload"),
     "p64_f32": Workload("p64_f32", 3, 64, _bw(64, {62: 0.75, 63: 0.5}), 1 << 24, 128, "f32",
                         "normal_zeros1pct", "two stragglers"),
     "p128_f32": Workload("p128_f32", 4, 128,
@@ -78,8 +82,8 @@ def make_rank(values: str, dtype: str, n: int, seed: int, device) -> torch.Tenso
     """One rank's input vector.
 
     normal            N(0, 1)
-    normal_1e-2       N(0, 1) * 1e-2, rounded to the dtype (bf16: torch's
-                      round-to-nearest-even)
+    normal_1e-2       N(0, 1) * 1e-2, rounded to the dtype (bf16, fp16:
+                      torch's round-to-nearest-even)
     normal_zeros1pct  N(0, 1), each element independently set to +0.0 with
                       probability 0.01
     student_t3_1e-3   z / sqrt(chi2_3 / 3) * 1e-3 with chi2_3 a sum of three

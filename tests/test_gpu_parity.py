@@ -2,7 +2,7 @@
 
 Every case compares every element of every rank bit for bit with the
 oracle's serial execution (fp32, bf16 and int32 alike: the schedule fixes the
-reduction order), from small ragged cases to the full-size workloads.  Slot
+reduction order; fp16 likewise), from small ragged cases to the full-size workloads.  Slot
 prefixes check that every step is materialised in its destination buffer,
 stage by stage.  Full-size runs also check properties that hold at any size
 (all ranks identical, exact int32 sums, the fp error bound) and sampled
@@ -15,7 +15,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import bits_equal, rand_inputs, to_device, to_host
+from gpu_util import bits_equal, int_view, rand_inputs, to_device, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +64,7 @@ def _run_both(o, p, slow, n, k, dtype, seed, kind="normal", slot_end=6, launches
     return x, ref, to_host(d, dtype)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 @pytest.mark.parametrize("p,slow", PROFILES)
 @pytest.mark.parametrize("n,k", SIZES)
 def test_small_bit_exact(o, dtype, p, slow, n, k):
@@ -75,7 +75,7 @@ def test_small_bit_exact(o, dtype, p, slow, n, k):
         assert (got == got[0][None, :]).all()
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 @pytest.mark.parametrize("p,slow", [(5, {0: 0.5}), (8, {7: 0.875}), (9, {0: 0.875, 3: 0.75, 8: 0.5}),
                                     (7, {}), (6, {1: 0.25, 2: 0.5})])
 @pytest.mark.parametrize("launches", [1, 0])
@@ -90,18 +90,22 @@ def test_stage_snapshots(o, dtype, p, slow, launches):
         assert bits_equal(got, ref), f"slots [0,{s})"
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("kind", ["denormal", "wide"])
+@pytest.mark.parametrize("dtype,kind", [(d, k) for d in ("f32", "bf16", "f16")
+                                         for k in ("denormal", "wide")] + [("f16", "overflow")])
 def test_special_values(o, dtype, kind):
-    """Subnormal inputs (no flush to zero on either side) and values spread
-    over 120 binades (heavy cancellation) stay bit-exact."""
+    """Subnormal inputs (no flush to zero on either side), values spread over
+    the format's binades (heavy cancellation) and, for fp16, partial sums
+    beyond the largest finite half (rounded to infinity on both sides) stay
+    bit-exact."""
     for p, slow in [(5, {0: 0.5}), (8, {7: 0.875}), (9, {0: 0.875, 3: 0.75, 8: 0.5})]:
         _say(f"case special {kind} dtype={dtype} p={p}")
         x, ref, got = _run_both(o, p, slow, 5000, 8, dtype, seed=3, kind=kind)
         assert bits_equal(got, ref)
+        if kind == "overflow":
+            assert np.isinf(oracle.f16_to_f64(got)).any()
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 def test_unaligned_buffers(o, dtype):
     """Rank buffers that are only element-aligned take the one-element path."""
     p, n, k = 8, 3000, 8
@@ -153,7 +157,8 @@ def _sample_coords(plan, n, rng, count=4096):
     return np.array(sorted(picks), dtype=np.int64)
 
 
-WORKLOADS = ["p4_f32", "p8_f32", "p8_i32", "p16_bf16", "p64_f32", "p128_f32"]
+WORKLOADS = ["p4_f32", "p8_f32", "p8_i32", "p16_bf16", "p16_f16", "p64_f32", "p128_f32"]
+UNIT = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}  # unit roundoff
 
 
 @pytest.mark.parametrize("name", WORKLOADS)
@@ -166,7 +171,7 @@ def test_workload_full_size(o, name):
     pl = o.optcc_plan(w.p, w.bandwidths, w.n, w.k)
     o.optcc_allreduce_emulate(x, w.p, w.n, w.dtype, pl)
     torch.cuda.synchronize()
-    iv = x.view(torch.int16) if w.dtype == "bf16" else x.view(torch.int32)
+    iv = int_view(x)
     for r in range(1, w.p):  # every rank holds the same bits
         assert torch.equal(iv[r], iv[0]), r
     rng = np.random.default_rng(1234)
@@ -188,8 +193,7 @@ def test_workload_full_size(o, name):
         else:
             xs = x0[:, c0:c1].to(torch.float64)
             err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
-            u = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8
-            assert bool((err <= w.p * u * xs.abs().sum(0)).all())
+            assert bool((err <= w.p * UNIT[w.dtype] * xs.abs().sum(0)).all())
     # and every element of every rank against the oracle's full serial run
     _say(f"case workload {name}: full oracle run")
     full = oracle.run(sched, w.dtype, to_host(x0, w.dtype).copy())
@@ -257,7 +261,7 @@ def test_graph_capture_replays(o):
     p, n, k = 8, 200000, 16
     bw = _bw(p, {7: 0.875})
     pl = o.optcc_plan(p, bw, n, k)
-    for dtype in ("f32", "bf16", "i32"):
+    for dtype in ("f32", "bf16", "i32", "f16"):
         x = rand_inputs(dtype, p, n, 31)
         d = to_device(x, dtype)
         d0 = d.clone()
@@ -280,8 +284,7 @@ def test_graph_capture_replays(o):
             torch.cuda.synchronize()
             g.replay()
             torch.cuda.synchronize()
-            assert torch.equal(d.view(torch.int16 if dtype == "bf16" else torch.int32),
-                               eager.view(torch.int16 if dtype == "bf16" else torch.int32))
+            assert torch.equal(int_view(d), int_view(eager))
         del g
 
 
@@ -343,7 +346,7 @@ def test_more_than_2g_elements_per_rank(o):
     assert bits_equal(to_host(x[:, idx], "i32"), cols)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 def test_fused_ranges_from_the_middle(o, dtype):
     """Any slot range [a, b), fused into one launch and started from the
     state after [0, a) (computed by the oracle), ends in the oracle's state

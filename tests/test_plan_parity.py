@@ -217,3 +217,5 @@ def test_traffic_accounting(o):
     # one launch per slot re-reads the state each slot starts from
     r6, w6 = pl.traffic("f32", launches=0)
     assert w6 == w and r6 > r
+    # 16-bit types move half the bytes of the same steps
+    assert pl.traffic("bf16") == pl.traffic("f16") == (r // 2, w // 2)
