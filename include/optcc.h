@@ -286,7 +286,10 @@ int optcc_plan_traffic(const optcc_plan_t *plan, optcc_dtype_t dtype, int slot_b
  *   - a flow starts after the earlier steps of its section that wrote its
  *     source's or its destination's range have finished (Sec. 3: a rank sends
  *     only data it holds);
- *   - work-conserving list scheduling in flow order;
+ *   - work-conserving list scheduling in priority order: flow order, except
+ *     that with several stragglers the segments are taken in groups of four
+ *     (one per pattern B, D, A', C'; the k/4 groups of App. D's time
+ *     analysis), group by group, each group in flow order;
  *   - server plans (App. E bandwidth model): a flow between two GPUs of one
  *     server runs over NVLink, on that GPU pair's own NVLink send/receive
  *     ports, at (g-1) times NIC speed: it lasts len/(g-1).

@@ -676,7 +676,16 @@ extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, i
 //    its source's range, or its destination's range, has finished (a rank
 //    sends only data it holds); a step finishes with its last flow;
 //  * list scheduling: whenever ports free up, ready flows are started in
-//    flow order (slot, segment, section, hop) if both their ports are free.
+//    priority order if both their ports are free.  Two priority orders are
+//    evaluated and the second schedule is kept only if it is shorter by more
+//    than a relative 1e-9:
+//      1. flow order (slot, segment, section, hop);
+//      2. pattern groups: the segments taken in groups, group by group,
+//         each group in flow order.  A group is four consecutive segments,
+//         one of each pattern (the k/4 groups of the time analyses of
+//         Sec. 4.3 and App. D); with several GPUs per server, eight
+//         consecutive segments of every part (App. E: the overlay needs
+//         8 | k), the parts' groups together.
 // Several GPUs per server (App. E bandwidth model): a flow between two GPUs of
 // one server runs over NVLink, on separate NVLink send/receive ports, at
 // (g-1) times NIC speed (len/(g-1)); flows between servers use the NICs.
@@ -697,6 +706,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     auto key = [](int rank, int seg, int sec) {
       return ((uint64_t)(uint32_t)rank << 40) | ((uint64_t)(uint32_t)seg << 12) | (uint64_t)(sec + 1);
     };
+    std::vector<int32_t> f_group;  // pattern group of the flow's segment
     for_each_step(*pl, [&](int, int g, int sec, int, int dst, const int *srcs, int ns,
                            int64_t, int64_t len) {
       const int64_t sid = (int64_t)st_dst.size();
@@ -717,6 +727,7 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
         f_src.push_back(2 * srcs[i] + (nvl ? 1 : 0));
         f_dst.push_back(2 * dst + (nvl ? 1 : 0));
         f_step.push_back(sid);
+        f_group.push_back(pl->g > 1 ? (g % pl->k) / 8 : g / 4);
         f_dur.push_back(nvl ? (double)len / (double)(pl->g - 1)
                             : (double)len * std::max(pl->ell[(size_t)srcs[i]], pl->ell[(size_t)dst]));
       }
@@ -724,91 +735,123 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     });
     st_first.push_back((int64_t)f_src.size());
     const int64_t nst = (int64_t)st_dst.size(), nfl = (int64_t)f_src.size();
-    std::vector<int32_t> pending((size_t)nst), left((size_t)nst);
     std::vector<std::vector<int64_t>> dependents((size_t)nst);
-    for (int64_t s = 0; s < nst; ++s) {
-      pending[(size_t)s] = (int32_t)deps[(size_t)s].size();
-      left[(size_t)s] = (int32_t)(st_first[(size_t)s + 1] - st_first[(size_t)s]);
-      for (int64_t d : deps[(size_t)s]) dependents[(size_t)d].push_back(s);
-    }
-    const int p = 2 * pl->p;  // ports
-    std::vector<double> fs((size_t)nfl, -1.0), ff((size_t)nfl, -1.0);
-    std::vector<char> send_busy((size_t)p, 0), recv_busy((size_t)p, 0);
-    // Ready flows by (sender, receiver).  Flows of one pair share both ports,
-    // so only the earliest of them in flow order can be the next to start.
-    std::vector<std::unordered_map<int, std::set<int64_t>>> out_ready((size_t)p);
-    std::vector<std::set<int>> in_partners((size_t)p);
-    using Ev = std::pair<double, int64_t>;
-    std::priority_queue<Ev, std::vector<Ev>, std::greater<Ev>> ev;
-    std::vector<int64_t> cand;
-    std::vector<int> freed_send, freed_recv;
-    auto make_ready = [&](int64_t s) {
-      for (int64_t f = st_first[(size_t)s]; f < st_first[(size_t)s + 1]; ++f) {
-        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
-        out_ready[(size_t)a][b].insert(f);
-        in_partners[(size_t)b].insert(a);
-        cand.push_back(f);
-      }
-    };
     for (int64_t s = 0; s < nst; ++s)
-      if (pending[(size_t)s] == 0) make_ready(s);
-    double t = 0.0, last = 0.0;
-    int64_t done = 0;
-    while (done < nfl) {
-      // candidates: newly ready flows and the head of every ready pair that
-      // touches a port freed at t; start them in flow order
-      for (int a : freed_send)
-        for (auto &kv : out_ready[(size_t)a])
-          if (!recv_busy[(size_t)kv.first]) cand.push_back(*kv.second.begin());
-      for (int b : freed_recv)
-        for (int a : in_partners[(size_t)b])
-          if (!send_busy[(size_t)a]) cand.push_back(*out_ready[(size_t)a][b].begin());
-      freed_send.clear();
-      freed_recv.clear();
-      std::sort(cand.begin(), cand.end());
-      cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
-      for (int64_t f : cand) {
-        if (fs[(size_t)f] >= 0.0) continue;
-        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
-        if (send_busy[(size_t)a] || recv_busy[(size_t)b]) continue;
-        auto &q = out_ready[(size_t)a][b];
-        if (q.empty() || *q.begin() != f) continue;  // an earlier flow of the pair is waiting
-        fs[(size_t)f] = t;
-        ff[(size_t)f] = t + f_dur[(size_t)f];
-        send_busy[(size_t)a] = 1;
-        recv_busy[(size_t)b] = 1;
-        q.erase(q.begin());
-        if (q.empty()) {
-          out_ready[(size_t)a].erase(b);
-          in_partners[(size_t)b].erase(a);
-        }
-        ev.push({ff[(size_t)f], f});
+      for (int64_t d : deps[(size_t)s]) dependents[(size_t)d].push_back(s);
+    const int p = 2 * pl->p;  // ports
+    // One list schedule: rk[f] = position of flow f in the priority order.
+    // Returns the makespan; fs/ff receive every flow's start and finish.
+    auto simulate = [&](const std::vector<int64_t> &rk, std::vector<double> &fs,
+                        std::vector<double> &ff) -> double {
+      std::vector<int64_t> order((size_t)nfl);
+      for (int64_t f = 0; f < nfl; ++f) order[(size_t)rk[(size_t)f]] = f;
+      std::vector<int32_t> pending((size_t)nst), left((size_t)nst);
+      for (int64_t s = 0; s < nst; ++s) {
+        pending[(size_t)s] = (int32_t)deps[(size_t)s].size();
+        left[(size_t)s] = (int32_t)(st_first[(size_t)s + 1] - st_first[(size_t)s]);
       }
-      cand.clear();
-      if (ev.empty()) return fail(OPTCC_EINVAL, "timeline: no flow can start (dependency cycle)");
-      t = ev.top().first;
-      const double tol = 1e-9 * std::max(1.0, t);
-      while (!ev.empty() && ev.top().first <= t + tol) {
-        const int64_t f = ev.top().second;
-        ev.pop();
-        ++done;
-        last = std::max(last, ff[(size_t)f]);
-        const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
-        send_busy[(size_t)a] = 0;
-        recv_busy[(size_t)b] = 0;
-        freed_send.push_back(a);
-        freed_recv.push_back(b);
-        const int64_t s = f_step[(size_t)f];
-        if (--left[(size_t)s] == 0)
-          for (int64_t d : dependents[(size_t)s])
-            if (--pending[(size_t)d] == 0) make_ready(d);
+      fs.assign((size_t)nfl, -1.0);
+      ff.assign((size_t)nfl, -1.0);
+      std::vector<char> send_busy((size_t)p, 0), recv_busy((size_t)p, 0);
+      // Ready flows by (sender, receiver), held as priority positions.  Flows
+      // of one pair share both ports, so only the first of them in priority
+      // order can be the next to start.  cand holds priority positions too.
+      std::vector<std::unordered_map<int, std::set<int64_t>>> out_ready((size_t)p);
+      std::vector<std::set<int>> in_partners((size_t)p);
+      using Ev = std::pair<double, int64_t>;
+      std::priority_queue<Ev, std::vector<Ev>, std::greater<Ev>> ev;
+      std::vector<int64_t> cand;
+      std::vector<int> freed_send, freed_recv;
+      auto make_ready = [&](int64_t s) {
+        for (int64_t f = st_first[(size_t)s]; f < st_first[(size_t)s + 1]; ++f) {
+          const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
+          out_ready[(size_t)a][b].insert(rk[(size_t)f]);
+          in_partners[(size_t)b].insert(a);
+          cand.push_back(rk[(size_t)f]);
+        }
+      };
+      for (int64_t s = 0; s < nst; ++s)
+        if (pending[(size_t)s] == 0) make_ready(s);
+      double t = 0.0, last = 0.0;
+      int64_t done = 0;
+      while (done < nfl) {
+        // candidates: newly ready flows and the head of every ready pair that
+        // touches a port freed at t; start them in priority order
+        for (int a : freed_send)
+          for (auto &kv : out_ready[(size_t)a])
+            if (!recv_busy[(size_t)kv.first]) cand.push_back(*kv.second.begin());
+        for (int b : freed_recv)
+          for (int a : in_partners[(size_t)b])
+            if (!send_busy[(size_t)a]) cand.push_back(*out_ready[(size_t)a][b].begin());
+        freed_send.clear();
+        freed_recv.clear();
+        std::sort(cand.begin(), cand.end());
+        cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
+        for (int64_t r : cand) {
+          const int64_t f = order[(size_t)r];
+          if (fs[(size_t)f] >= 0.0) continue;
+          const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
+          if (send_busy[(size_t)a] || recv_busy[(size_t)b]) continue;
+          auto &q = out_ready[(size_t)a][b];
+          if (q.empty() || *q.begin() != r) continue;  // an earlier flow of the pair is waiting
+          fs[(size_t)f] = t;
+          ff[(size_t)f] = t + f_dur[(size_t)f];
+          send_busy[(size_t)a] = 1;
+          recv_busy[(size_t)b] = 1;
+          q.erase(q.begin());
+          if (q.empty()) {
+            out_ready[(size_t)a].erase(b);
+            in_partners[(size_t)b].erase(a);
+          }
+          ev.push({ff[(size_t)f], f});
+        }
+        cand.clear();
+        if (ev.empty()) return -1.0;  // no flow can start: a dependency cycle
+        t = ev.top().first;
+        const double tol = 1e-9 * std::max(1.0, t);
+        while (!ev.empty() && ev.top().first <= t + tol) {
+          const int64_t f = ev.top().second;
+          ev.pop();
+          ++done;
+          last = std::max(last, ff[(size_t)f]);
+          const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
+          send_busy[(size_t)a] = 0;
+          recv_busy[(size_t)b] = 0;
+          freed_send.push_back(a);
+          freed_recv.push_back(b);
+          const int64_t s = f_step[(size_t)f];
+          if (--left[(size_t)s] == 0)
+            for (int64_t d : dependents[(size_t)s])
+              if (--pending[(size_t)d] == 0) make_ready(d);
+        }
+      }
+      return last;
+    };
+    // 1. flow order
+    std::vector<int64_t> rk((size_t)nfl);
+    for (int64_t f = 0; f < nfl; ++f) rk[(size_t)f] = f;
+    std::vector<double> fs, ff, fs2, ff2;
+    double best = simulate(rk, fs, ff);
+    if (best < 0.0) return fail(OPTCC_EINVAL, "timeline: no flow can start (dependency cycle)");
+    // 2. pattern groups (a stable counting sort of the flows by group)
+    const int ng = 1 + (nfl ? *std::max_element(f_group.begin(), f_group.end()) : 0);
+    if (ng > 1) {
+      std::vector<int64_t> pos((size_t)ng + 1, 0);
+      for (int64_t f = 0; f < nfl; ++f) ++pos[(size_t)f_group[(size_t)f] + 1];
+      for (int i = 0; i < ng; ++i) pos[(size_t)i + 1] += pos[(size_t)i];
+      for (int64_t f = 0; f < nfl; ++f) rk[(size_t)f] = pos[(size_t)f_group[(size_t)f]]++;
+      const double mk2 = simulate(rk, fs2, ff2);
+      if (mk2 >= 0.0 && mk2 < best * (1.0 - 1e-9)) {
+        best = mk2;
+        fs.swap(fs2);
+        ff.swap(ff2);
       }
     }
     for (int64_t f = 0; f < std::min(cap, nfl); ++f) {
       start[f] = fs[(size_t)f];
       finish[f] = ff[(size_t)f];
     }
-    *makespan = last;
+    *makespan = best;
   } catch (const std::bad_alloc &) {
     return fail(OPTCC_ENOMEM, "out of host memory");
   }

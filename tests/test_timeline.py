@@ -32,6 +32,8 @@ CASES = [
     (5, {0: 2 / 3}, 52 * 64 * 4, 4), (6, {2: 0.75}, 3000, 4), (8, {7: 0.875}, 64 * 7 * 8 * 4, 8),
     (7, {0: 0.5, 1: 0.75}, 64 * 5 * 8 * 4, 8), (9, {0: 0.875, 3: 0.75, 8: 0.5}, 4000, 4),
     (6, {5: 0.25}, 64 * 5 * 4, 4),
+    # several stragglers over three and four pattern groups (the group order wins)
+    (6, {1: 0.5, 4: 0.875}, 64 * 4 * 12 * 2, 12), (9, {2: 0.75, 5: 0.5, 6: 0.5}, 64 * 6 * 16, 16),
 ]
 
 
@@ -93,11 +95,14 @@ def test_validator_catches_planted_mistakes():
     assert any("dependency" in x for x in errs) and any("overlapping" in x for x in errs)
 
 
-@pytest.mark.parametrize("w", ["p4_f32", "p8_f32", "p16_bf16"])
+@pytest.mark.parametrize("w", ["p4_f32", "p8_f32", "p16_bf16", "p64_f32",
+                               pytest.param("p128_f32", marks=pytest.mark.slow)])
 def test_workload_evaluated_times(o, w):
     """Full-size evaluated makespans against the closed forms and bounds:
     p4 and p16 (l = 2) at or below (k+1)/k l n, p8 (bubble filling) within
-    1 % of its closed form; always above the best lower bound."""
+    1 % of its closed form, p64 and p128 (two and four stragglers, taken in
+    pattern groups) at or below (k+4) T_body (App. D); always above the best
+    lower bound."""
     from paper_2606_01680_amd.workloads import WORKLOADS
     W = WORKLOADS[w]
     pl = o.optcc_plan(W.p, W.bandwidths, W.n, W.k)
@@ -105,7 +110,7 @@ def test_workload_evaluated_times(o, w):
     closed = o.optcc_model_time(pl)
     lb = o.optcc_lower_bound(W.p, W.bandwidths, W.n)
     assert mk >= lb * (1 - 1e-12)
-    if pl.kind == "single_ge2":
+    if pl.kind in ("single_ge2", "multi"):
         assert mk <= closed * (1 + 1e-12)
     else:
         assert mk <= closed * 1.01
@@ -169,12 +174,12 @@ def test_server_validator_uses_nvlink_ports():
 @pytest.mark.parametrize("w", ["q4g4_bf16", "q16g4_f32"])
 def test_server_workload_evaluated_times(o, w):
     """Full-size server workloads: the evaluated makespan lies above the
-    tight multi-GPU bound (App. B.3) and within 40 % of the App. E closed
-    form (the greedy order does not reproduce the eight-row N-S overlay)."""
+    tight multi-GPU bound (App. B.3) and within 20 % of the App. E closed
+    form (list scheduling does not reproduce the eight-row N-S overlay)."""
     from paper_2606_01680_amd.workloads import WORKLOADS
     W = WORKLOADS[w]
     pl = o.optcc_plan_servers(W.q, W.g, W.bandwidths, W.n, W.k)
     mk, _, _ = pl.timeline(with_flows=False)
     lb = o.optcc_lower_bound_servers(W.q, W.g, W.bandwidths, W.n)
     closed = o.optcc_model_time(pl)
-    assert lb * (1 - 1e-12) <= mk <= 1.4 * closed
+    assert lb * (1 - 1e-12) <= mk <= 1.2 * closed
