@@ -67,6 +67,10 @@ struct KArgs {
   int32_t sb, se;  // slot range [sb, se)
   int32_t xcd_runs;  // 1: each XCD takes a contiguous run of tiles
   int32_t g;         // GPUs per server (1: one rank per server)
+  // launch setting, not read by the kernel: dynamic LDS bytes reserved per
+  // workgroup.  Reserving more than half of a CU's LDS holds the launch to
+  // one workgroup per CU.
+  int32_t occ_lds;
   // rank pointers.  g = 1: [0, pp) healthy ranks in ring order, [pp, pp+m)
   // stragglers sorted by slowdown (worst first).  g > 1: [h*g, h*g+g) the g
   // GPUs (by local index) of the h-th healthy server in ring order, then the

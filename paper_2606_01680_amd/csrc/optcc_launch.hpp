@@ -21,7 +21,7 @@ hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
   if constexpr (G == 0) {
     if (!vec16) {  // element-aligned buffers: one element per access
-      hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((optcc_exec_kernel<D, 1, 1, S, 0>), grid, block, (unsigned)a.occ_lds, st, a);
       return hipGetLastError();
     }
   } else if (!vec16) {
@@ -29,11 +29,11 @@ hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st) {
   }
   if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
     if (two) {
-      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S, G>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 2, S, G>), grid, block, (unsigned)a.occ_lds, st, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S, G>), grid, block, 0, st, a);
+  hipLaunchKernelGGL((optcc_exec_kernel<D, W16, 1, S, G>), grid, block, (unsigned)a.occ_lds, st, a);
   return hipGetLastError();
 }
 
