@@ -215,6 +215,22 @@ double optcc_lower_bound(int p, const double *link_bandwidths, int64_t N);
  */
 double optcc_lower_bound_servers(int q, int g, const double *server_bandwidths, int64_t N);
 
+/*
+ * optcc_narrow_f32 - round n fp32 values to dtype (OPTCC_BF16 or OPTCC_F16)
+ * with the rule every reduce step of the executor applies to its fp32 sum:
+ * round to nearest, ties to even; bf16 NaNs stay NaN (quietened, payload
+ * kept in the top bits), fp16 keeps subnormals and overflows to infinity.
+ * This is the per-step rounding of 16-bit data (Sec. 3 result applied to a
+ * 16-bit wire, one rounding per step), exposed so that it can be checked
+ * against an independent implementation over every fp32 pattern.
+ *   src    device array of n floats (4-byte aligned)
+ *   dst    device array of n 16-bit results (2-byte aligned); may not
+ *          overlap src
+ * Asynchronous on `stream`.  Errors: OPTCC_EINVAL (n < 0, NULL or misaligned
+ * pointers with n > 0, other dtypes), OPTCC_EDEVICE.
+ */
+int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dtype_t dtype, void *stream);
+
 /* Message of the last failure on the calling thread ("" if none). */
 const char *optcc_last_error(void);
 

@@ -24,7 +24,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result", f"-I{INCL
 
 KERNEL_TUS = ("optcc_exec.hip", "optcc_kern_f32.hip", "optcc_kern_bf16.hip", "optcc_kern_i32.hip",
               "optcc_kern_f16.hip", "optcc_kern_f32_g58.hip", "optcc_kern_bf16_g58.hip",
-              "optcc_kern_i32_g58.hip", "optcc_kern_f16_g58.hip")
+              "optcc_kern_i32_g58.hip", "optcc_kern_f16_g58.hip", "optcc_narrow.hip")
 
 
 def sources():

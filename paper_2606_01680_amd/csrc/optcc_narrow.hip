@@ -1,0 +1,51 @@
+// optcc_narrow_f32: the executor's per-step rounding rule applied to a plain
+// array, so that it can be compared with an independent implementation over
+// every fp32 bit pattern.  The element types (and with them the rounding
+// code) are the ones the fused kernel instantiates.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <string>
+
+#include "optcc_internal.hpp"
+#include "optcc_kernels.hpp"
+
+namespace optcc {
+namespace {
+
+template <class D>
+__global__ __launch_bounds__(256) void narrow_kernel(const float *__restrict__ src,
+                                                     typename D::S *__restrict__ dst, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = D::narrow(src[i]);
+}
+
+template <class D>
+hipError_t launch_narrow(const float *src, void *dst, int64_t n, hipStream_t st) {
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL((narrow_kernel<D>), dim3((unsigned)blocks), dim3(256), 0, st, src,
+                     static_cast<typename D::S *>(dst), n);
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace optcc
+
+extern "C" int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dtype_t dtype,
+                                void *stream) {
+  using namespace optcc;
+  set_error("");
+  if (n < 0) return fail(OPTCC_EINVAL, "n must be >= 0");
+  if (dtype != OPTCC_BF16 && dtype != OPTCC_F16)
+    return fail(OPTCC_EINVAL, "dtype must be OPTCC_BF16 or OPTCC_F16");
+  if (n == 0) return OPTCC_OK;
+  if (!src || !dst) return fail(OPTCC_EINVAL, "src and dst must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(src) % 4 || reinterpret_cast<uintptr_t>(dst) % 2)
+    return fail(OPTCC_EINVAL, "src and dst must be aligned to their element sizes");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t err = dtype == OPTCC_BF16 ? launch_narrow<kern::BF16>(src, dst, n, st)
+                                             : launch_narrow<kern::F16>(src, dst, n, st);
+  if (err != hipSuccess) return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));
+  return OPTCC_OK;
+}

@@ -28,7 +28,7 @@ EXPORTED = ("optcc_plan", "optcc_plan_servers", "optcc_plan_free", "optcc_allred
             "optcc_allreduce_emulate_slots", "optcc_model_time", "optcc_lower_bound",
             "optcc_lower_bound_servers", "optcc_last_error", "optcc_plan_info",
             "optcc_plan_segments", "optcc_plan_num_flows", "optcc_plan_get_flows",
-            "optcc_plan_traffic", "optcc_plan_timeline")
+            "optcc_plan_traffic", "optcc_plan_timeline", "optcc_narrow_f32")
 
 
 class PlanInfo(ctypes.Structure):
@@ -95,6 +95,8 @@ def _load():
     L.optcc_plan_traffic.restype = i32
     L.optcc_plan_timeline.argtypes = [vp, vp, vp, i64, ctypes.POINTER(dbl)]
     L.optcc_plan_timeline.restype = i32
+    L.optcc_narrow_f32.argtypes = [vp, vp, i64, i32, vp]
+    L.optcc_narrow_f32.restype = i32
     return L
 
 
@@ -308,3 +310,20 @@ def optcc_lower_bound_servers(q: int, g: int, server_bandwidths, N: int) -> floa
 
 def optcc_plan_timeline(plan: Plan):
     return plan.timeline()
+
+
+def optcc_narrow_f32(src, dst, dtype: str, stream=None) -> None:
+    """Round the fp32 device tensor `src` into the 16-bit device tensor `dst`
+    (same length) with the executor's per-step rounding rule for `dtype`
+    ("bf16" or "f16")."""
+    if dtype not in ("bf16", "f16"):
+        raise ValueError("dtype must be 'bf16' or 'f16'")
+    if src.element_size() != 4 or dst.element_size() != 2:
+        raise ValueError("src must hold 4-byte and dst 2-byte elements")
+    if not (src.is_cuda and dst.is_cuda and src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("src and dst must be contiguous GPU tensors")
+    if src.numel() != dst.numel():
+        raise ValueError("src and dst must have the same length")
+    _check(_lib.optcc_narrow_f32(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
+                                 int(src.numel()), DTYPES[dtype],
+                                 ctypes.c_void_p(_stream(stream))))

@@ -396,3 +396,33 @@ def test_binding_rejects_mismatched_tensors(o):
     with pytest.raises(ValueError, match="dtype"):
         o.optcc_allreduce_emulate(torch.zeros((p, n), device="cuda:0"), p, n, "f64", pl)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_narrowing_every_fp32_pattern(o, dtype):
+    """The executor's per-step rounding of an fp32 sum to bf16 / fp16 (round
+    to nearest even; fp16 subnormals and overflow to infinity), through the
+    library's optcc_narrow_f32, equals the oracle's C rule on all 2^32 fp32
+    bit patterns.  NaN inputs: bf16 bit for bit (both sides keep the top
+    payload bits and quieten), fp16 NaN for NaN (IEEE 754 leaves the payload
+    of a narrowed NaN open)."""
+    chunk = 1 << 27
+    round_ref = oracle.bf16_round if dtype == "bf16" else oracle.f16_round
+    out = torch.empty(chunk, dtype=torch.int16, device="cuda:0")
+    for c in range((1 << 32) // chunk):
+        if c % 8 == 0:
+            _say(f"case narrow {dtype} patterns from {c * chunk:#x}")
+        bits = np.arange(c * chunk, (c + 1) * chunk, dtype=np.int64).astype(np.uint32)
+        x = bits.view(np.float32)
+        want = round_ref(x)
+        d = torch.from_numpy(x).to("cuda:0")
+        o.optcc_narrow_f32(d, out, dtype)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().view(np.uint16)
+        nan_in = (bits & 0x7fffffff) > 0x7f800000
+        if dtype == "bf16":
+            assert np.array_equal(got, want), c
+        else:
+            assert np.array_equal(got[~nan_in], want[~nan_in]), c
+            g = got[nan_in]
+            assert bool((((g & 0x7c00) == 0x7c00) & ((g & 0x3ff) != 0)).all()), c

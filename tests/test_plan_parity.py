@@ -219,3 +219,14 @@ def test_traffic_accounting(o):
     assert w6 == w and r6 > r
     # 16-bit types move half the bytes of the same steps
     assert pl.traffic("bf16") == pl.traffic("f16") == (r // 2, w // 2)
+
+
+def test_narrow_argument_checks(o):
+    """optcc_narrow_f32 validates before touching the device: negative n,
+    other dtypes and NULL pointers are OPTCC_EINVAL; n = 0 is a no-op."""
+    L = o.lib()
+    assert L.optcc_narrow_f32(None, None, -1, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
+    assert L.optcc_narrow_f32(None, None, 4, o.DTYPES["f32"], None) == o.OPTCC_EINVAL
+    assert L.optcc_narrow_f32(None, None, 4, o.DTYPES["f16"], None) == o.OPTCC_EINVAL
+    assert "non-NULL" in o.optcc_last_error()
+    assert L.optcc_narrow_f32(None, None, 0, o.DTYPES["bf16"], None) == o.OPTCC_OK
