@@ -69,7 +69,9 @@ int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
 // Measured on MI355X: chains of more than 32 healthy ranks run 2.6-8 %
 // faster at one workgroup (4 waves) per CU than at the 4 workgroups their
 // registers allow (P' = 39, 47, 62, 95, 124); shorter chains gain nothing
-// and p = 8 loses 10 %.
+// and p = 8 loses 10 %.  Server plans of more than 32 ranks (with per-XCD
+// tile runs): q16g4 -1.5 %, q32g4 -6 %, 8x8 and 16x8 GPUs -2 to -4 %,
+// 32x2 and 64x2 +1 to +4 %.
 int one_workgroup_per_cu_lds() {
   static std::mutex mu;
   static std::map<int, int> cache;
@@ -147,13 +149,15 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   // short chains (inputs per lane: P' for one GPU per server, p for several):
-  // two vectors per lane and per-XCD tile runs (both measured faster up to
-  // 32 and neutral or slower beyond)
+  // two vectors per lane (measured faster up to 32 and neutral or slower
+  // beyond).  Per-XCD tile runs: for short chains and for every server plan
+  // (one GPU per server beyond 32: 0.6-0.9 % slower at p = 64/128; server
+  // plans beyond 32, together with one workgroup per CU: 2.4-27 % faster
+  // than with neither).  Longer chains run one workgroup per CU.
   const int chain = servers ? pl->p : pl->pp;
   const bool two = chain <= kTwoVectorMaxHealthy;
-  a.xcd_runs = chain <= kTwoVectorMaxHealthy ? 1 : 0;
-  // longer chains with one GPU per server: one workgroup per CU
-  a.occ_lds = !servers && !two ? one_workgroup_per_cu_lds() : 0;
+  a.xcd_runs = servers || chain <= kTwoVectorMaxHealthy ? 1 : 0;
+  a.occ_lds = two ? 0 : one_workgroup_per_cu_lds();
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
