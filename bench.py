@@ -152,6 +152,9 @@ def main():
                     help="time torch's plain device-to-device copy instead (the reference "
                          "kernel for scaling rocprofv3 byte counters)")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--n", type=int, default=None,
+                    help="elements per rank instead of the workload's own N (message-size "
+                         "sweeps); the line then reports that N and no counter traffic")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: the OptCC emulation runs the p logical ranks on ONE GPU; "
@@ -170,6 +173,12 @@ def main():
         copy_bench(torch, args)
         return
     w = WORKLOADS[args.workload]
+    if args.n is not None:
+        import dataclasses
+        if args.n < 1:
+            print("bench.py: --n must be >= 1", file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, n=args.n)
     x = make_inputs(w, device="cuda:0")
     x0 = x.clone()
     if w.g > 1:  # q servers of g GPUs (App. E)
@@ -225,7 +234,8 @@ def main():
         check = "pass" if ok else "FAIL"
 
     achieved = alg_bytes / (ms_launch * 1e-3) / 1e9
-    traffic = measured_traffic(w.name, args.launches)
+    # counter traffic was taken at the workload's own N
+    traffic = measured_traffic(w.name, args.launches) if args.n is None else None
     n = w.n
     t_model = optcc.optcc_model_time(plan) / n
     if w.g > 1:
