@@ -150,13 +150,15 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   hipStream_t st = static_cast<hipStream_t>(stream);
   // short chains (inputs per lane: P' for one GPU per server, p for several):
   // two vectors per lane (measured faster up to 32 and neutral or slower
-  // beyond).  Per-XCD tile runs: for short chains and for every server plan
-  // (one GPU per server beyond 32: 0.6-0.9 % slower at p = 64/128; server
-  // plans beyond 32, together with one workgroup per CU: 2.4-27 % faster
-  // than with neither).  Longer chains run one workgroup per CU.
+  // beyond).  Longer chains run one workgroup per CU.  Per-XCD tile runs:
+  // for short chains, for every server plan (beyond 32 ranks, together with
+  // one workgroup per CU, 2.4-27 % faster than with neither) and for longer
+  // one-GPU-per-server chains of at most kXcdRunsMaxTiles tiles (p = 64 and
+  // 128 at 2^20-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
+  // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower).
   const int chain = servers ? pl->p : pl->pp;
   const bool two = chain <= kTwoVectorMaxHealthy;
-  a.xcd_runs = servers || chain <= kTwoVectorMaxHealthy ? 1 : 0;
+  a.xcd_runs = servers || two || dt.ntiles <= kXcdRunsMaxTiles ? 1 : 0;
   a.occ_lds = two ? 0 : one_workgroup_per_cu_lds();
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {

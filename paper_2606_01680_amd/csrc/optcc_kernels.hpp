@@ -57,6 +57,9 @@ constexpr bool kNtMid = OPTCC_NT_MID;
 // ranks with one GPU per server, all p ranks with several) run two 16-byte
 // vectors per lane in lockstep (measured faster for short chains)
 constexpr int kTwoVectorMaxHealthy = 32;
+// longer one-GPU-per-server chains take per-XCD tile runs up to this many
+// tiles (measured faster at 2048 tiles and below, slower from 8192)
+constexpr int64_t kXcdRunsMaxTiles = 2048;
 
 struct KArgs {
   const TileDesc *tiles;
