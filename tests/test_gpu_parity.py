@@ -426,3 +426,50 @@ def test_narrowing_every_fp32_pattern(o, dtype):
             assert np.array_equal(got[~nan_in], want[~nan_in]), c
             g = got[nan_in]
             assert bool((((g & 0x7c00) == 0x7c00) & ((g & 0x3ff) != 0)).all()), c
+
+
+def test_threads_share_one_plan(o):
+    """A plan is shared read-only across host threads and streams: four
+    threads call a fresh plan at once (its device tables are uploaded on
+    first use under the plan's lock), each on its own stream and buffers,
+    and every result is bit-exact against the oracle."""
+    import threading
+    p, n, k = 9, 70000, 8
+    bw = _bw(p, {0: 0.875, 3: 0.75, 8: 0.5})
+    pl = o.optcc_plan(p, bw, n, k)
+    dts = ["f32", "bf16", "i32", "f16"]
+    xs = {dt: rand_inputs(dt, p, n, 300 + i) for i, dt in enumerate(dts)}
+    devs = {dt: to_device(xs[dt], dt) for dt in dts}
+    streams = {dt: torch.cuda.Stream() for dt in dts}
+    torch.cuda.synchronize()
+    errors = []
+    start = threading.Barrier(len(dts))
+
+    def work(dt):
+        try:
+            start.wait()
+            for it in range(3):  # repeated calls reuse the uploaded tables
+                with torch.cuda.stream(streams[dt]):
+                    d = devs[dt]
+                    o.optcc_allreduce_emulate(d, p, n, dt, pl, stream=streams[dt])
+                    streams[dt].synchronize()
+                    if it == 0:
+                        first = d.clone()
+                    d.copy_(to_device(xs[dt], dt))
+                    streams[dt].synchronize()
+            devs[dt] = first
+        except Exception as e:  # reported by the main thread
+            errors.append((dt, e))
+
+    _say("case threads sharing one plan")
+    ts = [threading.Thread(target=work, args=(dt,)) for dt in dts]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    sched = oracle.Schedule(p, bw, n, k)
+    for dt in dts:
+        ref = oracle.run(sched, dt, xs[dt].copy())
+        assert bits_equal(to_host(devs[dt], dt), ref), dt
