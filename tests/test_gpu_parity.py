@@ -473,3 +473,45 @@ def test_threads_share_one_plan(o):
     for dt in dts:
         ref = oracle.run(sched, dt, xs[dt].copy())
         assert bits_equal(to_host(devs[dt], dt), ref), dt
+
+
+def _random_case(rng):
+    """One random plan: ranks, stragglers and their bandwidths (NIC losses of
+    eighths or any fraction), N, k, element type; a fifth are server plans."""
+    dtype = ["f32", "bf16", "i32", "f16"][int(rng.integers(4))]
+    n = int(np.exp(rng.uniform(0.0, np.log(300000))))
+    def bandwidth():
+        return float(rng.integers(1, 8)) / 8 if rng.random() < 0.5 else float(rng.uniform(0.2, 0.999))
+    if rng.random() < 0.2:
+        q, g = int(rng.integers(3, 13)), int(rng.integers(2, 10))
+        bw = [1.0] * q
+        bw[int(rng.integers(q))] = bandwidth()
+        return dict(servers=(q, g), p=q * g, bw=bw, n=n, k=8 * int(rng.integers(3, 9)), dtype=dtype)
+    p = int(rng.integers(3, 73))
+    m = min(int(rng.choice([0, 1, 1, 1, 2, 3, 5])), p - 2)
+    bw = [1.0] * p
+    for r in rng.choice(p, size=m, replace=False):
+        bw[int(r)] = bandwidth()
+    return dict(servers=None, p=p, bw=bw, n=n, k=4 * int(rng.integers(1, 17)), dtype=dtype)
+
+
+def test_random_plans_bit_exact(o):
+    """200 seeded random plans of every kind, each bit for bit against the
+    oracle on every element of every rank."""
+    rng = np.random.default_rng(26060168)
+    for i in range(200):
+        c = _random_case(rng)
+        _say(f"case random #{i}: {c}")
+        if c["servers"] is None:
+            pl = o.optcc_plan(c["p"], c["bw"], c["n"], c["k"])
+            sched = oracle.Schedule(c["p"], c["bw"], c["n"], c["k"])
+        else:
+            q, g = c["servers"]
+            pl = o.optcc_plan_servers(q, g, c["bw"], c["n"], c["k"])
+            sched = oracle.Schedule.servers(q, g, c["bw"], c["n"], c["k"])
+        x = rand_inputs(c["dtype"], c["p"], c["n"], 1000 + i)
+        ref = oracle.run(sched, c["dtype"], x.copy())
+        d = to_device(x, c["dtype"])
+        o.optcc_allreduce_emulate(d, c["p"], c["n"], c["dtype"], pl)
+        torch.cuda.synchronize()
+        assert bits_equal(to_host(d, c["dtype"]), ref), i
