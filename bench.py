@@ -119,23 +119,30 @@ def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
                       f"serial C oracle, mean of {len(times)} run(s) of {t:.2f} s"}
 
 
-def copy_bench(torch, args):
-    """A plain copy of a known size: reads and writes copy_bytes each."""
-    src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda:0")
+def copy_rate(torch, nbytes, steps, warmup):
+    """(ms, GB/s read + write) of torch's plain device-to-device copy of
+    nbytes: the streaming ceiling of one read and one write stream."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
     dst = torch.empty_like(src)
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         dst.copy_(src)
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         dst.copy_(src)
     b.record()
     torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / args.steps
+    ms = a.elapsed_time(b) / steps
+    del src, dst
+    return ms, 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def copy_bench(torch, args):
+    """A plain copy of a known size: reads and writes copy_bytes each."""
+    ms, gbps = copy_rate(torch, args.copy_bytes, args.steps, args.warmup)
     print(json.dumps({"copy_bytes": args.copy_bytes, "ms": round(ms, 5),
-                      "GBps_read_plus_write": round(2 * args.copy_bytes / (ms * 1e-3) / 1e9, 2)}),
-          flush=True)
+                      "GBps_read_plus_write": round(gbps, 2)}), flush=True)
 
 
 def main():
