@@ -19,6 +19,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "achieved HBM GB/s of OptCC schedule execution (1 GPU) and % of peak BW"
 PEAK_GBPS = 8000.0  # MI355X HBM3E
+NIC_BYTES_PER_S = 25e9  # one healthy 200 Gb/s NIC, for the model times in seconds
 # device code of the executor (kernels, table layouts, launch choices)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2606_01680_amd", "csrc", f)
                for f in ("optcc_kernels.hpp", "optcc_internal.hpp", "optcc_launch.hpp",
@@ -287,6 +288,12 @@ def main():
                               "fault_free_ring_T0": round(t0_ring, 6),
                               "lower_bound": round(lb, 6),
                               "degraded_ring": round(float(max(plan.slowdowns)) * t0_ring, 6)},
+        # the same model times in seconds for this message on healthy
+        # 200 Gb/s NICs (25 GB/s, the paper's ConnectX-6 HDR setting)
+        "model_seconds_at_25GBps_nic": {
+            k: round(v * n * ESIZE[w.dtype] / NIC_BYTES_PER_S, 6)
+            for k, v in (("optcc", t_model), ("fault_free_ring_T0", t0_ring),
+                         ("lower_bound", lb))},
         "check": check,
         "kernel_sha256_16": kernel_hash(),
         "wall_s_timed": round(wall, 4),
