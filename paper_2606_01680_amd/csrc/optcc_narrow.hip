@@ -41,8 +41,10 @@ extern "C" int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dt
     return fail(OPTCC_EINVAL, "dtype must be OPTCC_BF16 or OPTCC_F16");
   if (n == 0) return OPTCC_OK;
   if (!src || !dst) return fail(OPTCC_EINVAL, "src and dst must be non-NULL");
-  if (reinterpret_cast<uintptr_t>(src) % 4 || reinterpret_cast<uintptr_t>(dst) % 2)
-    return fail(OPTCC_EINVAL, "src and dst must be aligned to their element sizes");
+  const uintptr_t s = reinterpret_cast<uintptr_t>(src), d = reinterpret_cast<uintptr_t>(dst);
+  if (s % 4 || d % 2) return fail(OPTCC_EINVAL, "src and dst must be aligned to their element sizes");
+  if (s < d + (uintptr_t)n * 2 && d < s + (uintptr_t)n * 4)
+    return fail(OPTCC_EINVAL, "src and dst overlap");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t err = dtype == OPTCC_BF16 ? launch_narrow<kern::BF16>(src, dst, n, st)
                                              : launch_narrow<kern::F16>(src, dst, n, st);

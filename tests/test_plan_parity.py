@@ -223,10 +223,15 @@ def test_traffic_accounting(o):
 
 def test_narrow_argument_checks(o):
     """optcc_narrow_f32 validates before touching the device: negative n,
-    other dtypes and NULL pointers are OPTCC_EINVAL; n = 0 is a no-op."""
+    other dtypes, NULL, misaligned and overlapping pointers are OPTCC_EINVAL;
+    n = 0 is a no-op."""
     L = o.lib()
     assert L.optcc_narrow_f32(None, None, -1, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
     assert L.optcc_narrow_f32(None, None, 4, o.DTYPES["f32"], None) == o.OPTCC_EINVAL
     assert L.optcc_narrow_f32(None, None, 4, o.DTYPES["f16"], None) == o.OPTCC_EINVAL
     assert "non-NULL" in o.optcc_last_error()
     assert L.optcc_narrow_f32(None, None, 0, o.DTYPES["bf16"], None) == o.OPTCC_OK
+    # checked before any launch: misaligned, overlapping
+    assert L.optcc_narrow_f32(0x1002, 0x9000, 4, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
+    assert L.optcc_narrow_f32(0x1000, 0x1008, 4, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
+    assert "overlap" in o.optcc_last_error()
