@@ -156,10 +156,13 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // one-GPU-per-server chains of at most kXcdRunsMaxTiles tiles (p = 64 and
   // 128 at 2^20-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
   // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower).
+  // bf16 keeps full occupancy: its integer rounding needs the ALU latency
+  // hiding of several waves (one workgroup per CU made p = 64/128 16-18 %
+  // and 16 x 4 servers 17-20 % slower; fp16, int32 and fp32 gain).
   const int chain = servers ? pl->p : pl->pp;
   const bool two = chain <= kTwoVectorMaxHealthy;
   a.xcd_runs = servers || two || dt.ntiles <= kXcdRunsMaxTiles ? 1 : 0;
-  a.occ_lds = two ? 0 : one_workgroup_per_cu_lds();
+  a.occ_lds = two || dtype == OPTCC_BF16 ? 0 : one_workgroup_per_cu_lds();
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
