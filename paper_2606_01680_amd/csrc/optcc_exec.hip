@@ -156,7 +156,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // one-GPU-per-server chains of at most kXcdRunsMaxTiles tiles (p = 64 and
   // 128 at 2^20-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
   // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower).
-  // bf16 keeps full occupancy: its integer rounding needs the ALU latency
+  // bf16 keeps full occupancy: eight elements per 16-byte vector, each
+  // widened by shifts, added in fp32 and rounded back, need the latency
   // hiding of several waves (one workgroup per CU made p = 64/128 16-18 %
   // and 16 x 4 servers 17-20 % slower; fp16, int32 and fp32 gain).
   const int chain = servers ? pl->p : pl->pp;

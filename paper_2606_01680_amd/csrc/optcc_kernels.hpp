@@ -99,12 +99,12 @@ struct BF16 {
   using S = uint16_t;
   using A = float;
   __device__ static A widen(S x) { return __uint_as_float((uint32_t)x << 16); }
-  // round to nearest, ties to even; NaN stays NaN
+  // round to nearest, ties to even, with gfx950's v_cvt_pk_bf16_f32; a NaN
+  // keeps its sign and top payload bits and is made quiet
   __device__ static S narrow(A f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (S)((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (S)(u >> 16);
+    const uint32_t u = __float_as_uint(f);
+    const S h = __builtin_bit_cast(uint16_t, (__bf16)f);
+    return (u & 0x7fffffffu) > 0x7f800000u ? (S)((u >> 16) | 0x0040u) : h;
   }
 };
 
