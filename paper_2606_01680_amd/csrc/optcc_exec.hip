@@ -18,25 +18,27 @@ namespace {
 
 using namespace kern;
 
-int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
+// The plan's tables for tiles of tile_elems elements on the current device,
+// uploaded on first use and cached.
+int device_tables(const optcc_plan_t &pl, int tile_elems, DeviceTables *out) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
   if (err != hipSuccess) return fail(OPTCC_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(err));
   std::lock_guard<std::mutex> lk(pl.mu);
-  auto it = pl.dev.find(dev);
+  auto it = pl.dev.find({dev, tile_elems});
   if (it != pl.dev.end()) {
     *out = it->second;
     return OPTCC_OK;
   }
-  // Tiles: 2048-element pieces of every segment's ring part and P2P chunk.
+  // Tiles: tile_elems-element pieces of every segment's ring part and P2P chunk.
   std::vector<TileDesc> tiles;
   for (int g = 0; g < pl.nseg; ++g) {
     const Segment &s = pl.seg[(size_t)g];
     auto cut = [&](int64_t b, int64_t e, int is_p2p) {
-      for (int64_t x = b; x < e; x += kTileElems) {
+      for (int64_t x = b; x < e; x += tile_elems) {
         TileDesc t;
         t.begin = x;
-        t.len = (int32_t)std::min<int64_t>(kTileElems, e - x);
+        t.len = (int32_t)std::min<int64_t>(tile_elems, e - x);
         t.meta = (g << 1) | is_p2p;
         tiles.push_back(t);
       }
@@ -59,7 +61,7 @@ int device_tables(const optcc_plan_t &pl, DeviceTables *out) {
                 std::string("uploading plan tables: ") + hipGetErrorString(err));
   }
   d.ntiles = (int64_t)tiles.size();
-  pl.dev[dev] = d;
+  pl.dev[{dev, tile_elems}] = d;
   *out = d;
   return OPTCC_OK;
 }
@@ -125,8 +127,19 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     if (ranges[i - 1].first + (uintptr_t)N * es > ranges[i].first)
       return fail(OPTCC_EINVAL, "rank buffers overlap");
 
+  // Tile length: 2048 elements, doubled (up to 8192) while a tile would move
+  // less than kTileMinBytes4/2 of algorithmic traffic (about 3p - 2
+  // accesses per element).  Measured with one straggler, 2 GiB of buffers,
+  // against 2048: fp32 p = 3 -7 % and p = 4 -3 % at 4096 (p = 5 +0.3 %);
+  // int32 p = 4 -4 %; bf16 p = 3 -18 % at 8192, p = 4 -11 % and p = 6
+  // -2 % at 4096, p = 7 +7 % and p = 8 +7 % at 4096; fp16 p = 4 -6 %,
+  // p = 8 +7 % at 4096.
+  int tile_elems = kTileElems;
+  const int64_t per_elem = (3 * (int64_t)p - 2) * (int64_t)es;
+  const int64_t min_bytes = es == 2 ? kTileMinBytes2 : kTileMinBytes4;
+  while (tile_elems < kTileElemsMax && (int64_t)tile_elems * per_elem < min_bytes) tile_elems *= 2;
   DeviceTables dt;
-  int rc = device_tables(*pl, &dt);
+  int rc = device_tables(*pl, tile_elems, &dt);
   if (rc != OPTCC_OK) return rc;
   KArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -205,7 +218,7 @@ extern "C" void optcc_plan_free(optcc_plan_t *pl) {
     int cur = -1;
     const bool have_dev = hipGetDevice(&cur) == hipSuccess;
     for (auto &kv : pl->dev) {
-      if (have_dev) (void)hipSetDevice(kv.first);
+      if (have_dev) (void)hipSetDevice(kv.first.first);
       (void)hipFree(kv.second.segs);
       (void)hipFree(kv.second.tiles);
     }

@@ -41,6 +41,12 @@ static_assert(sizeof(TileDesc) == 16, "TileDesc layout");
 constexpr int kQuantum = OPTCC_QUANTUM;
 constexpr int kTileQuanta = OPTCC_TILE_QUANTA;  // 2048 elements per tile by default
 constexpr int kTileElems = kQuantum * kTileQuanta;
+// Plans that move little per element take longer tiles, up to this many
+// elements, so that each workgroup moves at least kTileMinBytes4 (4-byte
+// elements) or kTileMinBytes2 (2-byte elements) of algorithmic traffic.
+constexpr int kTileElemsMax = 4 * kTileElems;
+constexpr int64_t kTileMinBytes4 = 96 << 10;
+constexpr int64_t kTileMinBytes2 = 72 << 10;
 
 struct DeviceTables {
   SegDesc *segs = nullptr;
@@ -69,11 +75,10 @@ struct optcc_plan {
   std::vector<int> strag;     // stragglers (servers when g > 1), l descending, ties lower
   std::vector<optcc::Segment> seg;
   std::vector<optcc::SegDesc> segdesc;
-  std::vector<optcc::TileDesc> tiles;
   int64_t num_steps = 0, num_flows = 0;
-  // device copies of segdesc/tiles, per device ordinal
+  // device copies of segdesc/tiles, per (device ordinal, tile length)
   mutable std::mutex mu;
-  mutable std::map<int, optcc::DeviceTables> dev;
+  mutable std::map<std::pair<int, int>, optcc::DeviceTables> dev;  // (device, tile elements)
 };
 
 namespace optcc {
