@@ -16,6 +16,10 @@ Parts (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
   with contributor sets: a REDUCE never counts a rank twice, and at the end
   every rank holds the contribution of every rank exactly once.
 * ``model``: the closed-form times and lower bounds, in exact rationals.
+* ``timeline``: the plan's flows timed in the paper's network model, in
+  exact rationals, and a validator of any timeline.
+* ``closed_form``: every coordinate's final value written directly from the
+  readings, without the step list, to check the step execution against.
 """
 from __future__ import annotations
 
