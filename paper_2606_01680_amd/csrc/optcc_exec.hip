@@ -173,10 +173,15 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // widened by shifts, added in fp32 and rounded back, need the latency
   // hiding of several waves (one workgroup per CU made p = 64/128 16-18 %
   // and 16 x 4 servers 17-20 % slower; fp16, int32 and fp32 gain).
+  // A single-hop chain (two healthy ranks, p = 3 with one straggler) runs
+  // one vector per lane in the identity order: 8 % faster than two vectors
+  // with XCD runs (p = 4 is fastest with both).
   const int chain = servers ? pl->p : pl->pp;
-  const bool two = chain <= kTwoVectorMaxHealthy;
-  a.xcd_runs = servers || two || dt.ntiles <= kXcdRunsMaxTiles ? 1 : 0;
-  a.occ_lds = two || dtype == OPTCC_BF16 ? 0 : one_workgroup_per_cu_lds();
+  const bool long_chain = chain > kTwoVectorMaxHealthy;
+  const bool single_hop = !servers && pl->pp == 2;
+  const bool two = !long_chain && !single_hop;
+  a.xcd_runs = servers || two || (long_chain && dt.ntiles <= kXcdRunsMaxTiles) ? 1 : 0;
+  a.occ_lds = long_chain && dtype != OPTCC_BF16 ? one_workgroup_per_cu_lds() : 0;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
