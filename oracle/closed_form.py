@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 The step-by-step executor (``oracle.run``) applies the schedule it builds;
 this module derives, for each coordinate, the expression the schedule must
-evaluate from the paper's stages and this build's readings, and evaluates it
+evaluate from the paper's stages and the readings listed below, and evaluates it
 with the same rounding rule.  The two agreeing bit for bit checks that the
 step list implements the readings.
 
