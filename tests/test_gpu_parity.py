@@ -515,3 +515,50 @@ def test_random_plans_bit_exact(o):
         o.optcc_allreduce_emulate(d, c["p"], c["n"], c["dtype"], pl)
         torch.cuda.synchronize()
         assert bits_equal(to_host(d, c["dtype"]), ref), i
+
+
+def test_one_graph_of_several_allreduces(o):
+    """Several AllReduces with different plans and element types (bubble
+    filling, several stragglers, a 40-rank chain launched at one workgroup
+    per CU, a server plan, fp16) captured in one HIP graph, as a training
+    step would capture its gradient buckets.  Every replay, with eager
+    restores and synchronisations in between, equals the oracle bit for bit."""
+    specs = [("one", 8, _bw(8, {7: 0.875}), None, 60000, 16, "f32"),
+             ("multi", 9, _bw(9, {0: 0.875, 3: 0.75, 8: 0.5}), None, 30000, 8, "bf16"),
+             ("long", 40, _bw(40, {5: 0.6}), None, 50000, 8, "f32"),
+             ("servers", 6, [1.0, 1.0, 0.5], (3, 2), 40000, 24, "i32"),
+             ("fp16", 5, _bw(5, {0: 0.5}), None, 20000, 8, "f16")]
+    cases = []
+    for name, p, bw, srv, n, k, dt in specs:
+        if srv is None:
+            pl, sched = o.optcc_plan(p, bw, n, k), oracle.Schedule(p, bw, n, k)
+        else:
+            pl = o.optcc_plan_servers(srv[0], srv[1], bw, n, k)
+            sched = oracle.Schedule.servers(srv[0], srv[1], bw, n, k)
+        x = rand_inputs(dt, p, n, 500 + p)
+        d = to_device(x, dt)
+        cases.append((name, p, n, dt, pl, oracle.run(sched, dt, x.copy()), d, d.clone()))
+    for name, p, n, dt, pl, ref, d, d0 in cases:  # first use: table upload
+        o.optcc_allreduce_emulate(d, p, n, dt, pl)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    for c in cases:
+        c[6].copy_(c[7])
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for name, p, n, dt, pl, ref, d, d0 in cases:
+                o.optcc_allreduce_emulate(d, p, n, dt, pl)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        _say(f"case one graph of several AllReduces rep={rep}")
+        for c in cases:
+            c[6].copy_(c[7])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for name, p, n, dt, pl, ref, d, d0 in cases:
+            assert bits_equal(to_host(d, dt), ref), (name, rep)
+    del g
