@@ -6,6 +6,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <exception>
+#include <future>
 #include <new>
 #include <queue>
 #include <set>
@@ -827,20 +829,26 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
       }
       return last;
     };
-    // 1. flow order
-    std::vector<int64_t> rk((size_t)nfl);
+    // 1. flow order; 2. pattern groups (a stable counting sort of the flows
+    // by group).  The two schedules share only read-only inputs, so the
+    // second runs on a thread of its own.
+    std::vector<int64_t> rk((size_t)nfl), rk2;
     for (int64_t f = 0; f < nfl; ++f) rk[(size_t)f] = f;
-    std::vector<double> fs, ff, fs2, ff2;
-    double best = simulate(rk, fs, ff);
-    if (best < 0.0) return fail(OPTCC_EINVAL, "timeline: no flow can start (dependency cycle)");
-    // 2. pattern groups (a stable counting sort of the flows by group)
     const int ng = 1 + (nfl ? *std::max_element(f_group.begin(), f_group.end()) : 0);
     if (ng > 1) {
       std::vector<int64_t> pos((size_t)ng + 1, 0);
       for (int64_t f = 0; f < nfl; ++f) ++pos[(size_t)f_group[(size_t)f] + 1];
       for (int i = 0; i < ng; ++i) pos[(size_t)i + 1] += pos[(size_t)i];
-      for (int64_t f = 0; f < nfl; ++f) rk[(size_t)f] = pos[(size_t)f_group[(size_t)f]]++;
-      const double mk2 = simulate(rk, fs2, ff2);
+      rk2.resize((size_t)nfl);
+      for (int64_t f = 0; f < nfl; ++f) rk2[(size_t)f] = pos[(size_t)f_group[(size_t)f]]++;
+    }
+    std::vector<double> fs, ff, fs2, ff2;
+    std::future<double> second;
+    if (ng > 1) second = std::async(std::launch::async, [&] { return simulate(rk2, fs2, ff2); });
+    double best = simulate(rk, fs, ff);
+    const double mk2 = ng > 1 ? second.get() : -1.0;  // rethrows the thread's exception
+    if (best < 0.0) return fail(OPTCC_EINVAL, "timeline: no flow can start (dependency cycle)");
+    if (ng > 1) {
       if (mk2 >= 0.0 && mk2 < best * (1.0 - 1e-9)) {
         best = mk2;
         fs.swap(fs2);
@@ -854,6 +862,8 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     *makespan = best;
   } catch (const std::bad_alloc &) {
     return fail(OPTCC_ENOMEM, "out of host memory");
+  } catch (const std::exception &e) {  // e.g. no thread for the second schedule
+    return fail(OPTCC_ENOMEM, std::string("timeline: ") + e.what());
   }
   return OPTCC_OK;
 }
