@@ -53,7 +53,7 @@ def test_servers(orc, q, g, slow, k):
         bw[s] = v
     for n in (1, 37, 2048 * 3 + 64 * 5 + 3, 30000):
         sched = oracle.Schedule.servers(q, g, bw, n, k)
-        for dtype in ("f32", "bf16"):
+        for dtype in ("f32", "bf16", "f16"):
             x = _inputs(dtype, q * g, n, q * 10 + g + n)
             got = oracle.run(sched, dtype, x.copy())
             want = cf.final_values_servers(dtype, x, q, g, bw, k)
