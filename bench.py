@@ -13,6 +13,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -282,7 +283,9 @@ def main():
             "traffic_frac": None if traffic is None else round(
                 traffic / (ms_launch * 1e-3) / 1e9 / PEAK_GBPS, 4),
             "algorithmic_bytes": alg_bytes, "read_bytes": rd, "write_bytes": wr,
-            "kernel_ms": round(ms_launch, 5), "kernel": "optcc_exec_kernel",
+            "kernel_ms": round(ms_launch, 5),
+            "kernel_ms_median": round(statistics.median(launch_ms), 5),
+            "kernel_ms_min": round(min(launch_ms), 5), "kernel": "optcc_exec_kernel",
         },
         "model_time_over_N": {"optcc": round(t_model, 6), "evaluated_schedule": evaluated,
                               "fault_free_ring_T0": round(t0_ring, 6),
