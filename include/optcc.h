@@ -227,7 +227,8 @@ double optcc_lower_bound_servers(int q, int g, const double *server_bandwidths, 
  *   dst    device array of n 16-bit results (2-byte aligned); may not
  *          overlap src
  * Asynchronous on `stream`.  Errors: OPTCC_EINVAL (n < 0, NULL, misaligned or
- * overlapping pointers with n > 0, other dtypes), OPTCC_EDEVICE.
+ * overlapping pointers with n > 0, an array that would run past the end of
+ * the address space, other dtypes), OPTCC_EDEVICE.
  */
 int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dtype_t dtype, void *stream);
 

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <string>
 
 #include "optcc_internal.hpp"
@@ -43,6 +44,8 @@ extern "C" int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dt
   if (!src || !dst) return fail(OPTCC_EINVAL, "src and dst must be non-NULL");
   const uintptr_t s = reinterpret_cast<uintptr_t>(src), d = reinterpret_cast<uintptr_t>(dst);
   if (s % 4 || d % 2) return fail(OPTCC_EINVAL, "src and dst must be aligned to their element sizes");
+  if ((uint64_t)n > (UINTPTR_MAX - s) / 4 || (uint64_t)n > (UINTPTR_MAX - d) / 2)
+    return fail(OPTCC_EINVAL, "n elements would run past the end of the address space");
   if (s < d + (uintptr_t)n * 2 && d < s + (uintptr_t)n * 4)
     return fail(OPTCC_EINVAL, "src and dst overlap");
   hipStream_t st = static_cast<hipStream_t>(stream);

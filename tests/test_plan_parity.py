@@ -223,8 +223,8 @@ def test_traffic_accounting(o):
 
 def test_narrow_argument_checks(o):
     """optcc_narrow_f32 validates before touching the device: negative n,
-    other dtypes, NULL, misaligned and overlapping pointers are OPTCC_EINVAL;
-    n = 0 is a no-op."""
+    other dtypes, NULL, misaligned and overlapping pointers and lengths past
+    the end of the address space are OPTCC_EINVAL; n = 0 is a no-op."""
     L = o.lib()
     assert L.optcc_narrow_f32(None, None, -1, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
     assert L.optcc_narrow_f32(None, None, 4, o.DTYPES["f32"], None) == o.OPTCC_EINVAL
@@ -235,3 +235,7 @@ def test_narrow_argument_checks(o):
     assert L.optcc_narrow_f32(0x1002, 0x9000, 4, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
     assert L.optcc_narrow_f32(0x1000, 0x1008, 4, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
     assert "overlap" in o.optcc_last_error()
+    # lengths whose byte ranges would wrap around the address space
+    assert L.optcc_narrow_f32(0x1000, 0x100000, 1 << 62, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
+    assert "address space" in o.optcc_last_error()
+    assert L.optcc_narrow_f32(0x1000, 0x100000, (1 << 63) - 1, o.DTYPES["f16"], None) == o.OPTCC_EINVAL
