@@ -76,6 +76,48 @@ def measured_traffic(workload: str, launches: int):
     return d.get("bytes_per_launch")
 
 
+# what each stage slot of the executor runs (one GPU per server; several)
+SLOT_NAMES = ["S3 of ordering 2: stragglers' values into the chain start",
+              "S1 reduce-scatter chain", "S2 upload; P2P up", "S3 download; P2P down",
+              "S4 allgather", "S2 of ordering 2: global sum to the stragglers"]
+SERVER_SLOT_NAMES = ["N3 collect on the straggler server (type 2)",
+                     "N1 collect on the healthy servers", "S3 into the chain start (type 2)",
+                     "S1 reduce-scatter chain", "S2 straggler leader adds (type 1)",
+                     "N2 fold on the straggler server (type 1)",
+                     "N3 copy back on the straggler server (type 1)",
+                     "S3 download (type 1)", "S4 allgather", "N4 distribute",
+                     "S2 download to the straggler leader (type 2)",
+                     "N2 distribute on the straggler server (type 2)"]
+
+
+def stage_breakdown(torch, optcc, x, w, plan, steps, warmup):
+    """Each stage slot timed on its own (one launch of that slot: a lane
+    loads the state its first step needs), with its algorithmic bytes."""
+    names = SERVER_SLOT_NAMES if w.g > 1 else SLOT_NAMES
+    E = torch.cuda.Event
+    out = []
+    for s in range(plan.num_slots):
+        rd, wr = plan.traffic(w.dtype, s, s + 1, 1)
+        if rd + wr == 0:
+            continue
+
+        def run():
+            optcc.optcc_allreduce_emulate_slots(x, w.p, w.n, w.dtype, plan, s, s + 1, 1)
+
+        for _ in range(warmup):
+            run()
+        evs = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(steps)]
+        for a, b in evs:
+            a.record()
+            run()
+            b.record()
+        torch.cuda.synchronize()
+        ms = statistics.median(a.elapsed_time(b) for a, b in evs)
+        out.append({"slot": s, "stage": names[s], "ms_median": round(ms, 5),
+                    "bytes": rd + wr, "GBps": round((rd + wr) / (ms * 1e-3) / 1e9, 2)})
+    return out
+
+
 def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
     """The oracle, untuned, on a bounded sample of whole segments (serial, one
     host thread), reported in the metric's unit.  When the whole workload
@@ -155,6 +197,8 @@ def main():
     ap.add_argument("--workload", default="p8_f32")
     ap.add_argument("--launches", type=int, default=1, choices=[0, 1],
                     help="1: fused (default); 0: one launch per stage slot")
+    ap.add_argument("--stages", action="store_true",
+                    help="also time every stage slot on its own (per-stage breakdown)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--copy-only", action="store_true",
@@ -221,6 +265,9 @@ def main():
     ms_step = ms_total / args.steps
     launch_ms = [a.elapsed_time(b) for a, b in evs]
     ms_launch = sum(launch_ms) / len(launch_ms)
+
+    stages = stage_breakdown(torch, optcc, x, w, plan, args.steps, args.warmup) if args.stages \
+        else None
 
     check = "skipped"
     if not args.no_check:  # the timed path computes the sum: properties at full size
@@ -301,6 +348,8 @@ def main():
         "kernel_sha256_16": kernel_hash(),
         "wall_s_timed": round(wall, 4),
     }
+    if stages is not None:
+        out["stages"] = stages
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x0, plan, alg_bytes)
     print(json.dumps(out), flush=True)
