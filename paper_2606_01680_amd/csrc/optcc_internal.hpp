@@ -47,6 +47,9 @@ constexpr int kTileElems = kQuantum * kTileQuanta;
 constexpr int kTileElemsMax = 4 * kTileElems;
 constexpr int64_t kTileMinBytes4 = 96 << 10;
 constexpr int64_t kTileMinBytes2 = 72 << 10;
+// Small messages take shorter tiles, down to one 16-byte vector per lane,
+// while the launch would have fewer than this many tiles.
+constexpr int64_t kTileMinCount = 1024;
 
 struct DeviceTables {
   SegDesc *segs = nullptr;

@@ -49,7 +49,8 @@ PROFILES = [
     (4, {0: 0.5, 1: 0.75}), (5, {1: 0.5, 2: 0.5, 3: 0.5}), (8, {2: 0.9999999}),
     (6, {5: 0.50000001}), (6, {5: 0.5}),
 ]
-# sizes span several 2048-element tiles, ragged tails, empty sections
+# sizes span several tiles (at these sizes 1024 elements for 4-byte types,
+# 2048 for 2-byte types), ragged tails, empty sections
 SIZES = [(1, 4), (37, 4), (64, 4), (1000, 8), (2048 * 3 + 64 * 5 + 3, 8), (40000, 12)]
 
 
@@ -73,6 +74,26 @@ def test_small_bit_exact(o, dtype, p, slow, n, k):
     assert bits_equal(got, ref)
     if n:
         assert (got == got[0][None, :]).all()
+
+
+@pytest.mark.parametrize("dtype,p,slow,n,k", [
+    # 2048-element tiles (two vectors per lane) with a sub-vector tail, and
+    # just below the size where they start (1024-element tiles)
+    ("f32", 8, {7: 0.875}, (1 << 21) + 2048 * 3 + 64 * 5 + 3, 64),
+    ("i32", 8, {7: 0.875}, (1 << 21) + 2048 * 3 + 64 * 5 + 3, 64),
+    ("f32", 8, {7: 0.875}, (1 << 21) - 64 * 3 + 1, 64),
+    # 4096-element tiles (fp32 p = 4; fp16 p = 6) and 8192 (bf16 p = 3)
+    ("f32", 4, {3: 0.5}, (1 << 22) + 5, 8),
+    ("f16", 6, {5: 0.5}, (1 << 22) + 2048 + 9, 16),
+    ("bf16", 3, {2: 0.5}, (1 << 23) + 77, 8),
+])
+def test_tile_lengths_bit_exact(o, dtype, p, slow, n, k):
+    """Every tile length the launch picks (1024 to 8192 elements: longer for
+    plans that move little per element, shorter for small messages), each
+    with ragged tiles at segment ends, bit for bit against the oracle."""
+    _say(f"case tiles dtype={dtype} p={p} slow={slow} n={n} k={k}")
+    x, ref, got = _run_both(o, p, slow, n, k, dtype, seed=5 * p + n % 97)
+    assert bits_equal(got, ref)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
