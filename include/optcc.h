@@ -18,9 +18,11 @@
  *     read-only device copy of its step tables per device it has run on.
  *   - "stream" is a hipStream_t (NULL = the default stream).  Emulation calls
  *     are asynchronous and return once the kernels are enqueued.  The first
- *     call of a plan on a device uploads its tables (hipMalloc + hipMemcpy);
- *     every later call only launches kernels and may be captured in a HIP
- *     graph.
+ *     call of a plan on a device with elements of a given size (2 or 4 bytes)
+ *     uploads its tables (hipMalloc + hipMemcpy) and so may not be captured
+ *     into a HIP graph (made during a capture, it fails with OPTCC_EINVAL
+ *     before touching the device and the capture stays valid); every later
+ *     call only launches kernels and may be captured.
  */
 #ifndef OPTCC_H
 #define OPTCC_H
@@ -139,8 +141,9 @@ void optcc_plan_free(optcc_plan_t *plan);
  * next step of the same section consumes is kept in registers.  The result is
  * bitwise deterministic.  With N = 0 (or an empty slot range) nothing is
  * read or written and the pointers are not inspected.  Errors: OPTCC_EINVAL
- * (mismatch with the plan, NULL
- * or misaligned pointers, overlapping buffers), OPTCC_EUNSUPPORTED
+ * (mismatch with the plan, NULL or misaligned pointers, overlapping buffers
+ * or buffers that would run past the end of the address space, a first call
+ * on a device made while `stream` is being captured), OPTCC_EUNSUPPORTED
  * (p > OPTCC_MAX_EMULATE_RANKS), OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the
  * plan on a device allocates its tables).
  */

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -19,8 +20,10 @@ namespace {
 using namespace kern;
 
 // The plan's tables for tiles of tile_elems elements on the current device,
-// uploaded on first use and cached.
-int device_tables(const optcc_plan_t &pl, int tile_elems, DeviceTables *out) {
+// uploaded on first use and cached.  The upload (hipMalloc, hipMemcpy) may
+// not run while `stream` is being captured into a graph: such a first call
+// fails before touching the device, and the capture stays valid.
+int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
   if (err != hipSuccess) return fail(OPTCC_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(err));
@@ -30,6 +33,11 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, DeviceTables *out) {
     *out = it->second;
     return OPTCC_OK;
   }
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone)
+    return fail(OPTCC_EINVAL,
+                "the stream is being captured and this plan's tables for this device and "
+                "element size are not uploaded yet: run the plan once outside the capture first");
   // Tiles: tile_elems-element pieces of every segment's ring part and P2P chunk.
   std::vector<TileDesc> tiles;
   for (int g = 0; g < pl.nseg; ++g) {
@@ -117,6 +125,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   for (int r = 0; r < p; ++r) {
     const uintptr_t a = reinterpret_cast<uintptr_t>(bufs[r]);
     if (!a) return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is NULL");
+    if (a > UINTPTR_MAX - (uintptr_t)N * es)
+      return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] + N elements would run past the end of the address space");
     if (a % es)
       return fail(OPTCC_EINVAL, "bufs[" + std::to_string(r) + "] is not aligned to the element size");
     if (a % 16) vec16 = false;
@@ -147,7 +157,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   const int vec_tile = kern::kThreads * (int)(16 / es);
   while (tile_elems > vec_tile && N / tile_elems < kTileMinCount) tile_elems /= 2;
   DeviceTables dt;
-  int rc = device_tables(*pl, tile_elems, &dt);
+  int rc = device_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt);
   if (rc != OPTCC_OK) return rc;
   KArgs a;
   std::memset(&a, 0, sizeof(a));

@@ -274,6 +274,44 @@ def test_empty_vector(o):
     torch.cuda.synchronize()
 
 
+def test_first_call_inside_capture_is_refused(o):
+    """A plan's first call on a device uploads its tables, so it cannot be
+    captured: made during a capture it raises OPTCC_EINVAL before touching
+    the device, the capture stays valid (the work around it replays), the
+    buffers are untouched, and an eager call afterwards gives the oracle's
+    result bit for bit."""
+    p, n, k = 8, 50000, 8
+    bw = _bw(p, {7: 0.875})
+    dtype = "f32"
+    x = rand_inputs(dtype, p, n, 41)
+    ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+    pl = o.optcc_plan(p, bw, n, k)
+    d = to_device(x, dtype)
+    d0 = d.clone()
+    side = torch.zeros(64, device="cuda:0")
+    torch.cuda.synchronize()
+    _say("case first call inside a capture")
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            side.add_(1.0)
+            with pytest.raises(o.OptccError) as e:
+                o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+            side.add_(2.0)
+    assert e.value.status == o.OPTCC_EINVAL
+    assert "captured" in str(e.value)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    assert (side == 3.0).all()
+    assert torch.equal(int_view(d), int_view(d0))
+    del g
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    assert bits_equal(to_host(d, dtype), ref)
+
+
 def test_graph_capture_replays(o):
     """After its first call on a device (which uploads the plan tables) an
     AllReduce is one kernel launch, so it can be captured in a HIP graph.

@@ -164,6 +164,10 @@ def test_errors(o):
     assert L.optcc_allreduce_emulate(ptrs, 4, 100, 0, pl.handle, None) == o.OPTCC_EINVAL
     ptrs = (ctypes.c_void_p * 4)(4097, 8192, 12288, 16384)
     assert L.optcc_allreduce_emulate(ptrs, 4, 100, 0, pl.handle, None) == o.OPTCC_EINVAL
+    # a buffer whose N elements would wrap around the address space
+    ptrs = (ctypes.c_void_p * 4)(4096, 8192, 12288, 2**64 - 256)
+    assert L.optcc_allreduce_emulate(ptrs, 4, 100, 0, pl.handle, None) == o.OPTCC_EINVAL
+    assert "address space" in o.optcc_last_error()
     ptrs = (ctypes.c_void_p * 4)(4096, 8192, 12288, 16384)
     assert L.optcc_allreduce_emulate_slots(ptrs, 4, 100, 0, pl.handle, 3, 2, 1, None) == o.OPTCC_EINVAL
     assert L.optcc_allreduce_emulate_slots(ptrs, 4, 100, 0, pl.handle, 0, 7, 1, None) == o.OPTCC_EINVAL
