@@ -187,10 +187,11 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // one-GPU-per-server chains of at most kXcdRunsMaxTiles tiles (p = 64 and
   // 128 at 2^20-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
   // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower).
-  // bf16 keeps full occupancy: eight elements per 16-byte vector, each
-  // widened by shifts, added in fp32 and rounded back, need the latency
-  // hiding of several waves (one workgroup per CU made p = 64/128 16-18 %
-  // and 16 x 4 servers 17-20 % slower; fp16, int32 and fp32 gain).
+  // bf16 with one GPU per server keeps full occupancy: eight elements per
+  // 16-byte vector, each widened by a shift, added in fp32 and rounded back,
+  // gain from the latency hiding of several waves (one workgroup per CU:
+  // p = 64 +0.5 %, p = 128 +1.5 %); bf16 server plans of more than 32 ranks
+  // gain from it (16 x 4 -3 %, 8 x 8 -1.3 %), like fp16, int32 and fp32.
   // A single-hop chain (two healthy ranks, p = 3 with one straggler) runs
   // one vector per lane in the identity order: 8 % faster than two vectors
   // with XCD runs (p = 4 is fastest with both).
@@ -199,7 +200,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   const bool single_hop = !servers && pl->pp == 2;
   const bool two = !long_chain && !single_hop;
   a.xcd_runs = servers || two || (long_chain && dt.ntiles <= kXcdRunsMaxTiles) ? 1 : 0;
-  a.occ_lds = long_chain && dtype != OPTCC_BF16 ? one_workgroup_per_cu_lds() : 0;
+  a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? one_workgroup_per_cu_lds() : 0;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;

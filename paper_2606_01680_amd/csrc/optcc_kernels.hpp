@@ -86,25 +86,31 @@ struct KArgs {
 struct F32 {
   using S = float;
   using A = float;
+  static constexpr bool kPairs = false;
   __device__ static A widen(S x) { return x; }
   __device__ static S narrow(A x) { return x; }
 };
 struct I32 {
   using S = uint32_t;  // two's complement adds wrap modulo 2^32
   using A = uint32_t;
+  static constexpr bool kPairs = false;
   __device__ static A widen(S x) { return x; }
   __device__ static S narrow(A x) { return x; }
 };
+// Narrowing rounds to nearest, ties to even, with gfx950's
+// v_cvt_pk_bf16_f32, which also gives a NaN the required result (sign and
+// top payload bits kept, made quiet): checked on all 2^32 fp32 patterns.
+// Vectors narrow two values per instruction (narrow_pair, low half first).
 struct BF16 {
   using S = uint16_t;
   using A = float;
+  static constexpr bool kPairs = true;
   __device__ static A widen(S x) { return __uint_as_float((uint32_t)x << 16); }
-  // round to nearest, ties to even, with gfx950's v_cvt_pk_bf16_f32; a NaN
-  // keeps its sign and top payload bits and is made quiet
-  __device__ static S narrow(A f) {
-    const uint32_t u = __float_as_uint(f);
-    const S h = __builtin_bit_cast(uint16_t, (__bf16)f);
-    return (u & 0x7fffffffu) > 0x7f800000u ? (S)((u >> 16) | 0x0040u) : h;
+  __device__ static S narrow(A f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+  __device__ static uint32_t narrow_pair(A lo, A hi) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){lo, hi}, b2));
   }
 };
 
@@ -114,6 +120,7 @@ struct BF16 {
 struct F16 {
   using S = uint16_t;
   using A = float;
+  static constexpr bool kPairs = false;
   __device__ static A widen(S x) { return (float)__builtin_bit_cast(_Float16, x); }
   __device__ static S narrow(A f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 };
@@ -183,8 +190,18 @@ __device__ __forceinline__ void st_mid(void *base, int64_t e, const Vec<D, W> &x
 template <class D, int W>
 __device__ __forceinline__ Vec<D, W> add2(const Vec<D, W> &a, const Vec<D, W> &b) {
   Vec<D, W> r;
+  if constexpr (D::kPairs && W % 2 == 0) {
 #pragma unroll
-  for (int i = 0; i < W; ++i) r.v[i] = D::narrow(D::widen(a.v[i]) + D::widen(b.v[i]));
+    for (int i = 0; i < W; i += 2) {
+      const uint32_t h = D::narrow_pair(D::widen(a.v[i]) + D::widen(b.v[i]),
+                                        D::widen(a.v[i + 1]) + D::widen(b.v[i + 1]));
+      r.v[i] = (typename D::S)h;
+      r.v[i + 1] = (typename D::S)(h >> 16);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; ++i) r.v[i] = D::narrow(D::widen(a.v[i]) + D::widen(b.v[i]));
+  }
   return r;
 }
 template <class D, int W>
@@ -206,8 +223,17 @@ __device__ __forceinline__ void accum(AccV<D, W> &acc, const Vec<D, W> &b) {
 template <class D, int W>
 __device__ __forceinline__ Vec<D, W> narrow(const AccV<D, W> &a) {
   Vec<D, W> r;
+  if constexpr (D::kPairs && W % 2 == 0) {
 #pragma unroll
-  for (int i = 0; i < W; ++i) r.v[i] = D::narrow(a.v[i]);
+    for (int i = 0; i < W; i += 2) {
+      const uint32_t h = D::narrow_pair(a.v[i], a.v[i + 1]);
+      r.v[i] = (typename D::S)h;
+      r.v[i + 1] = (typename D::S)(h >> 16);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; ++i) r.v[i] = D::narrow(a.v[i]);
+  }
   return r;
 }
 

@@ -14,12 +14,25 @@
 namespace optcc {
 namespace {
 
+// Types that narrow vectors two values at a time (D::kPairs) take pairs
+// through the same instruction as the executor, and an odd last element
+// through the single-value form.
 template <class D>
 __global__ __launch_bounds__(256) void narrow_kernel(const float *__restrict__ src,
                                                      typename D::S *__restrict__ dst, int64_t n) {
+  using S = typename D::S;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-    dst[i] = D::narrow(src[i]);
+  const int64_t first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if constexpr (D::kPairs) {
+    for (int64_t i = first; i < n / 2; i += stride) {
+      const uint32_t h = D::narrow_pair(src[2 * i], src[2 * i + 1]);
+      dst[2 * i] = (S)h;
+      dst[2 * i + 1] = (S)(h >> 16);
+    }
+    if ((n & 1) && first == 0) dst[n - 1] = D::narrow(src[n - 1]);
+  } else {
+    for (int64_t i = first; i < n; i += stride) dst[i] = D::narrow(src[i]);
+  }
 }
 
 template <class D>

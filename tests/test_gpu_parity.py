@@ -485,6 +485,21 @@ def test_narrowing_every_fp32_pattern(o, dtype):
             assert np.array_equal(got[~nan_in], want[~nan_in]), c
             g = got[nan_in]
             assert bool((((g & 0x7c00) == 0x7c00) & ((g & 0x3ff) != 0)).all()), c
+    # odd lengths: the last element goes through the single-value form
+    bits = np.array([0x7fa00001, 0xffc12345, 0x3f808000, 0x3f818000, 0x00000001,
+                     0x7f7fffff, 0xc0490fdb], dtype=np.uint32)
+    for n in (1, 3, 7):
+        x = bits[:n].view(np.float32)
+        want = round_ref(x)
+        d = torch.from_numpy(x.copy()).to("cuda:0")
+        o.optcc_narrow_f32(d, out[:n], dtype)
+        torch.cuda.synchronize()
+        got = out[:n].cpu().numpy().view(np.uint16)
+        nan_in = (bits[:n] & 0x7fffffff) > 0x7f800000
+        if dtype == "bf16":
+            assert np.array_equal(got, want), n
+        else:
+            assert np.array_equal(got[~nan_in], want[~nan_in]), n
 
 
 def test_threads_share_one_plan(o):
