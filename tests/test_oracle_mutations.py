@@ -1,0 +1,126 @@
+"""The oracle's pins catch plausible mistakes (CPU only).
+
+Each case plants one mistake in a copy of the oracle's C source (a wrong
+holder index, Stage 2 as a copy, a dropped straggler fold, an allgather one
+hop short, a point-to-point star missing a rank, the bubble-filling split
+rounded the wrong way), builds it with the same flags, and checks that the
+properties the paper fixes reject it: every rank ends with the exact int32
+sum (Sec. 3), and the bubble-filling split of the Sec. 4.2 / App. C example
+(golden fixture) with App. C's D rounded to the nearest whole quantum at
+other lengths.  The unmodified copy passes the same checks, so the checks
+are not failing for some other reason.
+"""
+import json
+import os
+import subprocess
+from fractions import Fraction as F
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import model
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+# (name, text in the oracle's source, replacement)
+MUTATIONS = [
+    ("holder index",
+     "int holder = ring_at(s, j, pp - 1);", "int holder = ring_at(s, j, pp - 2);"),
+    ("Stage 2 as a copy",
+     "rc |= push_step(s, 2, g, j, ORC_REDUCE, fin, one, 1, off, len);",
+     "rc |= push_step(s, 2, g, j, ORC_COPY, fin, one, 1, off, len);"),
+    ("straggler fold dropped",
+     "if (npre > 0) rc |= push_step(s, 0,", "if (0) rc |= push_step(s, 0,"),
+    ("allgather one hop short",
+     "for (int t = 0; t <= pp - 2; ++t) {\n    one[0] = ring_at(s, j, t - 1);",
+     "for (int t = 0; t <= pp - 3; ++t) {\n    one[0] = ring_at(s, j, t - 1);"),
+    ("P2P star misses a rank",
+     "push_step(s, 2, g, -1, ORC_REDUCE, st, s->ring, s->pp, off, len);",
+     "push_step(s, 2, g, -1, ORC_REDUCE, st, s->ring, s->pp - 1, off, len);"),
+    ("bubble split rounded down",
+     "dq = (int64_t)floor(x + 0.5);", "dq = (int64_t)floor(x);"),
+]
+
+PROFILES = [(5, {0: 0.5}), (8, {7: 0.875}), (6, {0: 0.5, 5: 0.75}), (9, {0: 0.875, 3: 0.75, 8: 0.5})]
+
+
+def _bw(p, slow):
+    b = [1.0] * p
+    for r, v in slow.items():
+        b[r] = v
+    return b
+
+
+def _int32_sums_hold():
+    """Sec. 3: every rank ends with the elementwise sum (int32 wraps exactly)."""
+    for p, slow in PROFILES:
+        for n, k in [(1000, 4), (64 * 41 + 7, 8)]:
+            rng = np.random.default_rng(11 * p + n)
+            x = rng.integers(-(2**31), 2**31, size=(p, n), dtype=np.int64).astype(np.int32)
+            want = (x.astype(np.int64).sum(0) + 2**31) % 2**32 - 2**31
+            y = oracle.run(oracle.Schedule(p, _bw(p, slow), n, k), "i32", x.copy())
+            if not (y.astype(np.int64) == want[None, :]).all():
+                return False
+    return True
+
+
+def _bubble_example_holds():
+    """Sec. 4.2 / App. C at p = 5, l = 1.5, k = 4: P2P chunks of D = n/52 and
+    sections of s' = 3n/52 when n is 52 quanta."""
+    g = json.load(open(os.path.join(GOLD, "bubble_example_p5_l1.5.json")))
+    p, k, ell = g["p"], g["k"], F(g["ell"])
+    sp, d = model.bubble_split(p, ell, 1, k)
+    n = 52 * 64
+    s = oracle.Schedule(p, g["bandwidths"], n, k)
+    for seg in range(k):
+        if s.p2p_len[seg] != d * n:
+            return False
+        secs = {st["sec"]: st["len"] for st in s.steps() if st["seg"] == seg and st["sec"] >= 0}
+        if set(secs.values()) != {sp * n}:
+            return False
+    # at other lengths each P2P chunk is App. C's D in whole quanta, rounded
+    # to the nearest (within half a quantum of the real value)
+    for p, b, k, lq in [(5, 2 / 3, 4, 11), (8, 0.875, 4, 10), (16, 0.75, 8, 23)]:
+        bw = [1.0] * (p - 1) + [b]
+        ell = 1 / F(b).limit_denominator(10**6)
+        _, d = model.bubble_split(p, ell, 1, k)
+        s = oracle.Schedule(p, bw, 64 * k * lq, k)
+        for seg in range(k):
+            if abs(F(s.p2p_len[seg], 64) - d * k * lq) > F(1, 2):
+                return False
+    return True
+
+
+def _build(tmp_path, name, src):
+    c = tmp_path / f"{name}.c"
+    so = tmp_path / f"lib{name}.so"
+    c.write_text(src)
+    subprocess.run(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-shared",
+                    "-fPIC", "-o", str(so), str(c), "-lm"], check=True)
+    return str(so)
+
+
+def _checks_with(monkeypatch, so):
+    monkeypatch.setattr(oracle, "_LIB", so)
+    monkeypatch.setattr(oracle, "_lib", None)
+    try:
+        return _int32_sums_hold() and _bubble_example_holds()
+    except oracle.OracleError:
+        return False
+
+
+@pytest.fixture(scope="module")
+def source():
+    return open(oracle._SRC).read()
+
+
+def test_unmodified_copy_passes(tmp_path, monkeypatch, source):
+    assert _checks_with(monkeypatch, _build(tmp_path, "control", source))
+
+
+@pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_planted_mistake_is_caught(tmp_path, monkeypatch, source, name, old, new):
+    assert source.count(old) == 1, f"mutation site of {name!r} not found once"
+    so = _build(tmp_path, "m" + str(abs(hash(name)) % 10**8), source.replace(old, new))
+    assert not _checks_with(monkeypatch, so), f"{name}: not caught"
