@@ -113,6 +113,7 @@ class Schedule:
         if rc != 0:
             raise OracleError(rc, L.orc_last_error().decode())
         self._h = h
+        self._L = L  # the library that owns the handle frees it
         info = np.zeros(12, np.int64)
         ring = np.zeros(max(p, 1), np.int32)
         strag = np.zeros(max(p, 1), np.int32)
@@ -140,8 +141,9 @@ class Schedule:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None and _lib is not None:
-            _lib.orc_free(h)
+        L = getattr(self, "_L", None)
+        if h is not None and L is not None:
+            L.orc_free(h)
             self._h = None
 
     def steps(self):
@@ -149,7 +151,7 @@ class Schedule:
         ints = np.zeros((max(self.nsteps, 1), 6), np.int32)
         offs = np.zeros((max(self.nsteps, 1), 3), np.int64)
         pool = np.zeros(max(self.npool, 1), np.int32)
-        lib().orc_steps(self._h, _ptr(ints), _ptr(offs), _ptr(pool))
+        self._L.orc_steps(self._h, _ptr(ints), _ptr(offs), _ptr(pool))
         out = []
         for i in range(self.nsteps):
             slot, seg, sec, op, dst, nsrc = (int(v) for v in ints[i])
@@ -171,9 +173,9 @@ def run(sched: Schedule, dtype: str, bufs: np.ndarray, slot_lo=0, slot_hi=NUM_SE
             and bufs.dtype == NP_DTYPES[dtype]):
         raise ValueError("bufs must be a C-contiguous [p, N] array of the dtype")
     ptrs = (ctypes.c_void_p * sched.p)(*[bufs[r].ctypes.data for r in range(sched.p)])
-    rc = lib().orc_run(sched._h, DTYPES[dtype], ptrs, int(slot_lo), int(slot_hi))
+    rc = sched._L.orc_run(sched._h, DTYPES[dtype], ptrs, int(slot_lo), int(slot_hi))
     if rc != 0:
-        raise OracleError(rc, lib().orc_last_error().decode())
+        raise OracleError(rc, sched._L.orc_last_error().decode())
     return bufs
 
 
@@ -186,10 +188,10 @@ def run_sampled(sched: Schedule, dtype: str, cols: np.ndarray, coords: np.ndarra
             and cols.dtype == NP_DTYPES[dtype]):
         raise ValueError("cols must be a C-contiguous [p, S] array of the dtype")
     ptrs = (ctypes.c_void_p * sched.p)(*[cols[r].ctypes.data for r in range(sched.p)])
-    rc = lib().orc_run_sampled(sched._h, DTYPES[dtype], ptrs, _ptr(coords), coords.size,
+    rc = sched._L.orc_run_sampled(sched._h, DTYPES[dtype], ptrs, _ptr(coords), coords.size,
                                int(slot_lo), int(slot_hi))
     if rc != 0:
-        raise OracleError(rc, lib().orc_last_error().decode())
+        raise OracleError(rc, sched._L.orc_last_error().decode())
     return cols
 
 
