@@ -161,6 +161,25 @@ def test_server_small_bit_exact(o, dtype, q, g, slow, n, k):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("dtype,q,g,slow,n,k", [
+    # 2048-element tiles, two vectors per lane, a sub-vector tail
+    ("f32", 4, 2, {3: 0.5}, (1 << 21) + 2048 * 3 + 64 * 5 + 3, 24),
+    ("i32", 4, 2, {3: 0.5}, (1 << 21) + 2048 * 3 + 64 * 5 + 3, 24),
+    # 4096-element tiles (2-byte elements, six ranks)
+    ("bf16", 3, 2, {2: 0.5}, (1 << 22) + 77, 24),
+    ("f16", 3, 2, {0: 0.875}, (1 << 22) + 2048 + 9, 24),
+])
+def test_server_tile_lengths_bit_exact(o, dtype, q, g, slow, n, k):
+    """Server plans at sizes where the launch takes 2048- or 4096-element
+    tiles (the small-message rule does not shorten them), bit for bit
+    against the oracle."""
+    from gpu_util import bits_equal
+    _say(f"case servers tiles dtype={dtype} q={q} g={g} slow={slow} n={n} k={k}")
+    x, ref, got = _run_both(o, q, g, slow, n, k, dtype, seed=q * 100 + g * 10 + n % 89)
+    assert bits_equal(got, ref)
+
+
+@pytest.mark.gpu
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 @pytest.mark.parametrize("q,g,slow", [(3, 2, {2: 0.5}), (4, 3, {1: 0.875}), (5, 4, {0: 0.5})])
 @pytest.mark.parametrize("launches", [1, 0])
