@@ -130,7 +130,9 @@ void optcc_plan_free(optcc_plan_t *plan);
  *
  *   bufs   host array of p device pointers; bufs[r] holds rank r's N elements
  *          of `dtype`, aligned to the element size.  Buffers must not overlap.
- *          16-byte alignment of every pointer enables the vector path.
+ *          16-byte alignment of every pointer enables the vector path;
+ *          128-byte (cache-line) alignment gives full speed (16-byte-only
+ *          alignment costs 3-24 %, element alignment 1.4-3.6x).
  *   p, N   must equal the plan's
  *   dtype  OPTCC_F32 (fp32 adds), OPTCC_BF16 and OPTCC_F16 (IEEE binary16)
  *          (fp32 accumulation, one round-to-nearest-even per step; fp16
