@@ -2,8 +2,9 @@
 // sequences and the kernel.  Included through optcc_launch.hpp.
 //
 // The p logical ranks are p buffers in HBM.  One workgroup takes one tile of
-// 2048 consecutive elements of one segment's ring sections (or of its
-// point-to-point chunk) and runs, lane by lane, every step of the schedule
+// consecutive elements (1024 to 8192, 2048 for most plans; the launch picks
+// the length) of one segment's ring sections (or of its point-to-point
+// chunk) and runs, lane by lane, every step of the schedule
 // that touches those elements, in the section's own stage order: the
 // partial sum a hop forwards stays in registers, and every step still writes
 // its destination rank's buffer.  All arithmetic is elementwise, so the work
