@@ -12,7 +12,7 @@ Parts (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
   executed serially step by step in plain C (``optcc_oracle.c``).
 * ``brute_sum``: the definition of the result (Sec. 3, problem setting): the
   elementwise sum over ranks, in fp64 (int64 for int32, wrapped mod 2**32).
-* ``provenance``: the correctness conditions of Sec. 3 checked symbolically
+* ``provenance`` / ``provenance_steps``: the correctness conditions of Sec. 3 checked symbolically
   with contributor sets: a REDUCE never counts a rank twice, and at the end
   every rank holds the contribution of every rank exactly once.
 * ``model``: the closed-form times and lower bounds, in exact rationals.
@@ -258,15 +258,23 @@ def tolerance(dtype: str, p: int, bufs: np.ndarray) -> np.ndarray:
 
 
 def provenance(sched: Schedule, n_small: int | None = None):
-    """Symbolic execution with contributor sets (bitmasks over ranks).
+    """Symbolic execution of a schedule with contributor sets; see
+    ``provenance_steps``."""
+    n = sched.n if n_small is None else n_small
+    return provenance_steps(sched.p, n, sched.steps())
 
-    Returns (ok, message).  Checks, for every coordinate: a REDUCE adds sets
-    that are disjoint from the destination's and from each other (nothing is
-    counted twice), and at the end every rank holds all p contributions."""
-    p, n = sched.p, sched.n if n_small is None else n_small
+
+def provenance_steps(p: int, n: int, steps):
+    """Symbolic execution with contributor sets (bitmasks over ranks) of a
+    step list in serial order (dicts with op, dst, srcs, off, len).
+
+    Returns (ok, message).  Checks, for every coordinate below n: a REDUCE
+    adds sets that are disjoint from the destination's and from each other
+    (nothing is counted twice), and at the end every rank holds all p
+    contributions (Sec. 3: every rank ends with the sum of all inputs)."""
     full = (1 << p) - 1
     held = [[1 << r for _ in range(n)] for r in range(p)]
-    for st in sched.steps():
+    for st in steps:
         for c in range(st["off"], min(st["off"] + st["len"], n)):
             if st["op"] == COPY:
                 held[st["dst"]][c] = held[st["srcs"][0]][c]

@@ -124,3 +124,43 @@ def test_planted_mistake_is_caught(tmp_path, monkeypatch, source, name, old, new
     assert source.count(old) == 1, f"mutation site of {name!r} not found once"
     so = _build(tmp_path, "m" + str(abs(hash(name)) % 10**8), source.replace(old, new))
     assert not _checks_with(monkeypatch, so), f"{name}: not caught"
+
+
+# ---------------------------------------------------------------- time model
+# Planted mistakes in a copy of oracle/model.py: each body count off by a
+# fraction of a body, and the l < 2 branch without its head/tail term.  The
+# hand-evaluated golden values at finite k (tests/golden/model_values.json)
+# must reject every one.
+MODEL_MUTATIONS = [
+    ("App. D body count k+3", "return (k + 4) * body", "return (k + 3) * body"),
+    ("App. E body count k+5", "(k + F(11, 2))", "(k + 5)"),
+    ("Sec. 4.3 body count k", "ell * n * F(k + 1, k)", "ell * n"),
+    ("App. C head/tail dropped", "* (k + ell - 1) / k", "* k / k"),
+    ("App. D extra sections dropped", "(ells[0] * (p - m) + 2 * (m - 1)) * s",
+     "(ells[0] * (p - m)) * s"),
+]
+
+
+def _model_copy(tmp_path, name, text):
+    import importlib.util
+    path = tmp_path / f"model_{name}.py"
+    path.write_text(text)
+    spec = importlib.util.spec_from_file_location(f"model_{name}", str(path))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_unmodified_model_copy_passes(tmp_path):
+    from test_model_golden import model_failures
+    text = open(model.__file__).read()
+    assert model_failures(_model_copy(tmp_path, "control", text)) == []
+
+
+@pytest.mark.parametrize("name,old,new", MODEL_MUTATIONS, ids=[m[0] for m in MODEL_MUTATIONS])
+def test_planted_model_mistake_is_caught(tmp_path, name, old, new):
+    from test_model_golden import model_failures
+    text = open(model.__file__).read()
+    assert text.count(old) == 1, f"mutation site of {name!r} not found once"
+    mod = _model_copy(tmp_path, "m" + str(abs(hash(name)) % 10**8), text.replace(old, new))
+    assert model_failures(mod), f"{name}: not caught"
