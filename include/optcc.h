@@ -118,8 +118,12 @@ int optcc_plan(int p, const double *link_bandwidths, int64_t N, int n_chunks,
 int optcc_plan_servers(int q, int g, const double *server_bandwidths, int64_t N, int n_chunks,
                        optcc_plan_t **out);
 
-/* Free a plan and its device tables.  The caller guarantees that no emulation
- * using it is still running on any stream.  NULL is ignored. */
+/* Free a plan and its device tables (the plan was built by optcc_plan or
+ * optcc_plan_servers, whose passages define it).  The caller guarantees that
+ * no emulation using it is still running on any stream, and that every HIP
+ * graph that captured an emulation call of this plan has been destroyed
+ * first: a graph keeps the addresses of the plan's device tables, so
+ * replaying it after the free would read freed memory.  NULL is ignored. */
 void optcc_plan_free(optcc_plan_t *plan);
 
 /*
@@ -146,8 +150,11 @@ void optcc_plan_free(optcc_plan_t *plan);
  * (mismatch with the plan, NULL or misaligned pointers, overlapping buffers
  * or buffers that would run past the end of the address space, a first call
  * on a device made while `stream` is being captured), OPTCC_EUNSUPPORTED
- * (p > OPTCC_MAX_EMULATE_RANKS), OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the
- * plan on a device allocates its tables).
+ * (p > OPTCC_MAX_EMULATE_RANKS, or a segment whose ring sections hold 2^31
+ * or more quanta: the device tables index a segment's quanta in 32 bits;
+ * that is N of about 2^39 elements per rank at k = 4, beyond one GPU's HBM),
+ * OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the plan on a device allocates
+ * its tables).  These checks are made before any device call.
  */
 int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
                             const optcc_plan_t *plan, void *stream);
@@ -237,7 +244,9 @@ double optcc_lower_bound_servers(int q, int g, const double *server_bandwidths, 
  */
 int optcc_narrow_f32(const float *src, void *dst, int64_t n, optcc_dtype_t dtype, void *stream);
 
-/* Message of the last failure on the calling thread ("" if none). */
+/* Message of the last failure on the calling thread ("" if none).  Library
+ * plumbing, not part of the method: every entry point above sets it when it
+ * returns an error status (or NaN) and clears it on entry to an emulation. */
 const char *optcc_last_error(void);
 
 /* ------------------------------------------------------------ introspection
@@ -266,12 +275,42 @@ int optcc_plan_info(const optcc_plan_t *plan, optcc_plan_info_t *info, int32_t *
 int optcc_plan_segments(const optcc_plan_t *plan, int64_t *offset, int64_t *length,
                         int64_t *p2p_length);
 
+/* The paper's stage of a flow.  Sec. 4.1 splits every section's AllReduce
+ * into four NIC stages: S1 reduce-scatter over the healthy ring, S2 upload
+ * to the straggler, S3 download from the straggler, S4 allgather over the
+ * healthy ring (ordering 2 runs them S3-S1-S4-S2, so S3 is then the
+ * straggler's raw value going out first).  Bubble filling enlarges the S2
+ * and S3 flows with a point-to-point chunk (App. C), so its up and down
+ * flows carry S2 and S3.  App. E adds the NVLink phases N1 collect, N2
+ * distribute or fold, N3 collect or copy back, N4 distribute around them.
+ * Stage of each executor slot:
+ *   one GPU per server:   slot 0 S3, 1 S1, 2 S2, 3 S3, 4 S4, 5 S2
+ *   several per server:   slot 0 N3, 1 N1, 2 S3, 3 S1, 4 S2, 5 N2, 6 N3,
+ *                         7 S3, 8 S4, 9 N4, 10 S2, 11 N2 */
+#define OPTCC_STAGE_S1 1
+#define OPTCC_STAGE_S2 2
+#define OPTCC_STAGE_S3 3
+#define OPTCC_STAGE_S4 4
+#define OPTCC_STAGE_N1 5
+#define OPTCC_STAGE_N2 6
+#define OPTCC_STAGE_N3 7
+#define OPTCC_STAGE_N4 8
+
+/* One flow: a point-to-point transfer of one section (or one bubble-filling
+ * chunk) from one rank to another (Sec. 4.1 defines a flow this way; App. E
+ * adds NVLink flows between the GPUs of one server).  A step is one
+ * destination write: a reduce step with several sources has one flow per
+ * source, all with the same step index. */
 typedef struct {
   int32_t slot;    /* 0..num_slots-1, see optcc_allreduce_emulate_slots */
   int32_t segment; /* 0..num_segments-1 */
   int32_t section; /* 0..P'-1, or -1 for the point-to-point chunk */
   int32_t op;      /* 0 copy, 1 reduce (dst += src) */
   int32_t src, dst;
+  int32_t stage;   /* OPTCC_STAGE_*: the paper's stage the flow belongs to */
+  int32_t hop;     /* position of the step among its section's steps in this
+                      slot, from 0 (the hop along a chain: S1 and S4, the
+                      NVLink rings) */
   int64_t step;    /* index of the step: the sources of a multi-source reduce
                       share it and are listed in accumulation order */
   int64_t offset, length; /* element range */

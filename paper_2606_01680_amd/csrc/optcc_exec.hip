@@ -136,6 +136,12 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   for (size_t i = 1; i < ranges.size(); ++i)
     if (ranges[i - 1].first + (uintptr_t)N * es > ranges[i].first)
       return fail(OPTCC_EINVAL, "rank buffers overlap");
+  // The device tables index a segment's ring quanta in 32 bits (SegDesc,
+  // section_of): refuse a plan whose segments would not fit.
+  for (const Segment &s : pl->seg)
+    if (s.qbase * (int64_t)pl->pp + s.nbig > (int64_t)INT32_MAX)
+      return fail(OPTCC_EUNSUPPORTED, "a segment's ring sections hold 2^31 or more quanta; use "
+                                      "more segments (n_chunks) or a smaller N");
 
   // Tile length: 2048 elements, doubled (up to 8192) while a tile would move
   // less than kTileMinBytes4/2 of algorithmic traffic (about 3p - 2

@@ -523,12 +523,32 @@ extern "C" int64_t optcc_plan_num_flows(const optcc_plan_t *pl) {
   return pl->num_flows;
 }
 
+// The paper's stage (OPTCC_STAGE_*) of each executor slot: Sec. 4.1 stages
+// S1-S4 (bubble filling rides on S2 and S3, App. C) and App. E's NVLink
+// phases N1-N4.
+static const int kSlotStage[OPTCC_NUM_SLOTS] = {OPTCC_STAGE_S3, OPTCC_STAGE_S1, OPTCC_STAGE_S2,
+                                                OPTCC_STAGE_S3, OPTCC_STAGE_S4, OPTCC_STAGE_S2};
+static const int kServerSlotStage[OPTCC_NUM_SERVER_SLOTS] = {
+    OPTCC_STAGE_N3, OPTCC_STAGE_N1, OPTCC_STAGE_S3, OPTCC_STAGE_S1, OPTCC_STAGE_S2, OPTCC_STAGE_N2,
+    OPTCC_STAGE_N3, OPTCC_STAGE_S3, OPTCC_STAGE_S4, OPTCC_STAGE_N4, OPTCC_STAGE_S2, OPTCC_STAGE_N2};
+
 extern "C" int64_t optcc_plan_get_flows(const optcc_plan_t *pl, optcc_flow_t *out, int64_t cap) {
   if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
   if (cap > 0 && !out) return fail(OPTCC_EINVAL, "out is NULL");
+  const int *stage_of = pl->kind == OPTCC_KIND_SERVERS ? kServerSlotStage : kSlotStage;
   int64_t nf = 0, step = 0;
+  int last_slot = -1, last_seg = -1, last_sec = -2, hop = 0;
   for_each_step(*pl, [&](int slot, int g, int sec, int op, int dst, const int *srcs, int ns,
                          int64_t off, int64_t len) {
+    // steps arrive grouped by (slot, segment, section), hop by hop
+    if (slot == last_slot && g == last_seg && sec == last_sec) {
+      ++hop;
+    } else {
+      hop = 0;
+      last_slot = slot;
+      last_seg = g;
+      last_sec = sec;
+    }
     for (int i = 0; i < ns; ++i, ++nf) {
       if (nf >= cap) continue;
       optcc_flow_t &f = out[nf];
@@ -538,6 +558,8 @@ extern "C" int64_t optcc_plan_get_flows(const optcc_plan_t *pl, optcc_flow_t *ou
       f.op = op;
       f.src = srcs[i];
       f.dst = dst;
+      f.stage = stage_of[slot];
+      f.hop = hop;
       f.step = step;
       f.offset = off;
       f.length = len;

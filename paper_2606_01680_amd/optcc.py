@@ -42,7 +42,10 @@ class PlanInfo(ctypes.Structure):
 
 FLOW_DTYPE = np.dtype([("slot", np.int32), ("segment", np.int32), ("section", np.int32),
                        ("op", np.int32), ("src", np.int32), ("dst", np.int32),
+                       ("stage", np.int32), ("hop", np.int32),
                        ("step", np.int64), ("offset", np.int64), ("length", np.int64)])
+# the paper's stages (optcc_flow_t.stage)
+STAGE_NAMES = {1: "S1", 2: "S2", 3: "S3", 4: "S4", 5: "N1", 6: "N2", 7: "N3", 8: "N4"}
 
 
 class OptccError(RuntimeError):
@@ -97,6 +100,9 @@ def _load():
     L.optcc_plan_timeline.restype = i32
     L.optcc_narrow_f32.argtypes = [vp, vp, i64, i32, vp]
     L.optcc_narrow_f32.restype = i32
+    # the HIP runtime the library is linked against (found through its handle)
+    L.hipStreamIsCapturing.argtypes = [vp, ctypes.POINTER(i32)]
+    L.hipStreamIsCapturing.restype = i32
     return L
 
 
@@ -204,7 +210,24 @@ def optcc_plan_servers(q: int, g: int, server_bandwidths, N: int, n_chunks: int)
     return Plan(h)
 
 
+# Plans whose emulation calls were captured into a HIP graph.  A graph keeps
+# the addresses of the plan's device tables, so such a plan is kept alive
+# (never freed by garbage collection) until release_captured_plans() is
+# called, which the caller does once every graph that captured it has been
+# destroyed.
+_captured_plans: dict = {}
+
+
+def release_captured_plans() -> None:
+    """Drop the references kept for plans used under graph capture.  Call
+    it only after destroying every HIP graph that captured one of them."""
+    _captured_plans.clear()
+
+
 def optcc_plan_free(plan: Plan) -> None:
+    if id(plan) in _captured_plans:
+        raise RuntimeError("this plan was used inside a HIP graph capture: destroy the graphs "
+                           "that captured it and call release_captured_plans() first")
     h = plan._h
     plan._h = None
     if h is not None:
@@ -264,20 +287,33 @@ def _stream(stream):
     return int(getattr(stream, "cuda_stream", stream))
 
 
+def _keep_if_captured(plan: Plan, stream: int) -> None:
+    """Keep `plan` alive if the call just made on `stream` was captured."""
+    status = ctypes.c_int(0)
+    if _lib.hipStreamIsCapturing(ctypes.c_void_p(stream), ctypes.byref(status)) == 0 \
+            and status.value != 0:
+        _captured_plans[id(plan)] = plan
+
+
 def optcc_allreduce_emulate(bufs, p: int, N: int, dtype: str, plan: Plan, stream=None) -> None:
     """Run the whole schedule in place (one fused launch) on `stream`
-    (default: torch's current stream)."""
+    (default: torch's current stream).  A call captured into a HIP graph
+    keeps `plan` alive (see release_captured_plans)."""
     arr = _ptr_array(bufs, p, int(N), dtype)
+    st = _stream(stream)
     _check(_lib.optcc_allreduce_emulate(arr, int(p), int(N), DTYPES[dtype], plan.handle,
-                                        ctypes.c_void_p(_stream(stream))))
+                                        ctypes.c_void_p(st)))
+    _keep_if_captured(plan, st)
 
 
 def optcc_allreduce_emulate_slots(bufs, p: int, N: int, dtype: str, plan: Plan, slot_begin: int,
                                   slot_end: int, launches: int = 1, stream=None) -> None:
     arr = _ptr_array(bufs, p, int(N), dtype)
+    st = _stream(stream)
     _check(_lib.optcc_allreduce_emulate_slots(arr, int(p), int(N), DTYPES[dtype], plan.handle,
                                               int(slot_begin), int(slot_end), int(launches),
-                                              ctypes.c_void_p(_stream(stream))))
+                                              ctypes.c_void_p(st)))
+    _keep_if_captured(plan, st)
 
 
 def optcc_model_time(plan: Plan, link_bandwidths=None) -> float:

@@ -347,6 +347,46 @@ def test_graph_capture_replays(o):
         del g
 
 
+def test_captured_plan_outlives_its_python_reference(o):
+    """A plan whose call was captured into a graph stays alive when the
+    caller drops it (its device tables are still in the graph): replays
+    after garbage collection give the eager result; freeing it explicitly is
+    refused until release_captured_plans()."""
+    import gc
+    p, n, k = 8, 100000, 8
+    bw = _bw(p, {7: 0.875})
+    dtype = "f32"
+    x = rand_inputs(dtype, p, n, 47)
+    ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+    d = to_device(x, dtype)
+    d0 = d.clone()
+    pl = o.optcc_plan(p, bw, n, k)
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)  # first use: table upload
+    torch.cuda.synchronize()
+    assert bits_equal(to_host(d, dtype), ref)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    with pytest.raises(RuntimeError):
+        o.optcc_plan_free(pl)
+    del pl
+    gc.collect()
+    for rep in range(3):
+        _say(f"case captured plan after its reference is dropped rep={rep}")
+        d.copy_(d0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert bits_equal(to_host(d, dtype), ref)
+    del g
+    torch.cuda.synchronize()
+    o.release_captured_plans()
+    gc.collect()
+
+
 def test_every_small_length(o):
     """Every length from 0 to 200 and around each tile and quantum boundary up
     to three tiles, for one straggler (bubble filling), several stragglers

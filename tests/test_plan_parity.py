@@ -243,3 +243,68 @@ def test_narrow_argument_checks(o):
     assert L.optcc_narrow_f32(0x1000, 0x100000, 1 << 62, o.DTYPES["bf16"], None) == o.OPTCC_EINVAL
     assert "address space" in o.optcc_last_error()
     assert L.optcc_narrow_f32(0x1000, 0x100000, (1 << 63) - 1, o.DTYPES["f16"], None) == o.OPTCC_EINVAL
+
+
+@pytest.mark.parametrize("p,slow", PROFILES)
+def test_flow_stages_follow_the_stage_definitions(o, p, slow):
+    """Every exported flow names the paper's stage it belongs to (Sec. 4.1:
+    S1 and S4 run between healthy ranks, S2 ends at a straggler, S3 starts
+    at one; bubble filling rides on S2 and S3, App. C), and `hop` counts the
+    steps of a section within its slot: the S1 chain and the S4 allgather
+    have P' - 1 hops each."""
+    bw = _bw(p, slow)
+    pl = o.optcc_plan(p, bw, 64 * 97 + 5, 8)
+    strag = set(int(r) for r in pl.stragglers)
+    fl = pl.flows()
+    assert set(np.unique(fl["stage"])) <= {1, 2, 3, 4}
+    for f in fl:
+        st, src, dst = int(f["stage"]), int(f["src"]), int(f["dst"])
+        if st in (1, 4):
+            assert src not in strag and dst not in strag
+            assert int(f["op"]) == (1 if st == 1 else 0)
+        elif st == 2:
+            assert dst in strag and src not in strag
+        else:
+            assert src in strag and dst not in strag
+    ring = fl[(fl["section"] >= 0) & np.isin(fl["stage"], [1, 4])]
+    for slot in (1, 4):
+        hops = ring["hop"][ring["slot"] == slot]
+        if hops.size:
+            assert hops.min() == 0 and hops.max() == pl.healthy - 2
+            assert np.bincount(hops).tolist() == [hops.size // (pl.healthy - 1)] * (pl.healthy - 1)
+
+
+@pytest.mark.parametrize("q,g,sb", [(3, 2, {1: 0.5}), (4, 4, {0: 0.5}), (5, 3, {4: 0.875})])
+def test_server_flow_stages(o, q, g, sb):
+    """App. E: NVLink phases N1-N4 run between GPUs of one server, NIC stages
+    S1-S4 between servers; S2 ends on the straggler server, S3 leaves it."""
+    bw = [1.0] * q
+    for s, v in sb.items():
+        bw[s] = v
+    pl = o.optcc_plan_servers(q, g, bw, 64 * 24 * 7 + 3, 24)
+    sv = int(pl.stragglers[0])
+    fl = pl.flows()
+    assert set(np.unique(fl["stage"])) == set(range(1, 9))
+    for f in fl:
+        st, a, b = int(f["stage"]), int(f["src"]) // g, int(f["dst"]) // g
+        if st >= 5:
+            assert a == b
+        else:
+            assert a != b
+            assert (b == sv) == (st == 2) and (a == sv) == (st == 3)
+
+
+def test_segment_quanta_beyond_32_bits_refused(o):
+    """The device tables index a segment's ring quanta in 32 bits: a plan
+    whose segment holds 2^31 quanta or more is refused with
+    OPTCC_EUNSUPPORTED before any device call (the pointers are never
+    dereferenced).  Only refused cases are run here: an accepted one would
+    go on to the device."""
+    L = o.lib()
+    for p, bw, k, nq in [(3, [1.0] * 3, 4, 4 * 2**31), (5, [1.0] * 4 + [0.5], 8, 8 * (2**31 + 5)),
+                         (3, [1.0] * 3, 4, 4 * 2**31 + 3)]:
+        n = 64 * nq
+        pl = o.optcc_plan(p, bw, n, k)
+        ptrs = (ctypes.c_void_p * p)(*[(r + 1) << 45 for r in range(p)])
+        rc = L.optcc_allreduce_emulate(ptrs, p, n, 2, pl.handle, None)
+        assert rc == o.OPTCC_EUNSUPPORTED and "quanta" in o.optcc_last_error()
