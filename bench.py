@@ -3,9 +3,13 @@
 
 One step = one call of optcc_allreduce_emulate over a whole workload: every
 step of the OptCC schedule for p rank buffers resident in HBM (one fused
-kernel launch).  Prints one JSON line.
+kernel launch).  Prints one JSON line.  The headline is the p = 8 workload
+(one of eight NICs lost on one rank); the default run also measures every
+headline configuration the same way (p4_f32, p8_f32, p8_i32, p16_bf16,
+p64_f32, p128_f32) and reports them under "configs".
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload p8_f32]
+    python bench.py --trace-summary kernel_trace.csv --line bench_line.json
 """
 from __future__ import annotations
 
@@ -118,11 +122,39 @@ def stage_breakdown(torch, optcc, x, w, plan, steps, warmup):
     return out
 
 
-def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
-    """The oracle, untuned, on a bounded sample of whole segments (serial, one
-    host thread), reported in the metric's unit.  When the whole workload
-    runs in less than the budget it is run again (inputs restored, untimed)
-    until the budget is spent, and the mean is reported."""
+def host_info():
+    """CPU model, logical CPUs of the host and CPUs this process may use."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
+
+
+def oracle_threads():
+    """Threads for the all-cores leg: OMP_NUM_THREADS when set (the CPU
+    share of the process), else every CPU this process may use."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return int(env)
+    return host_info()["usable_cpus"]
+
+
+def cpu_leg(w, x0, plan, traffic_bytes, budget_s, threads):
+    """The oracle, untuned, on a bounded sample of whole segments, reported in
+    the metric's unit (algorithmic bytes of the sample / oracle time).
+    threads = 1: the serial C executor; otherwise the same steps on
+    `threads` OpenMP threads (bit-identical results).  When the whole
+    workload runs in less than the budget it is run again (inputs restored,
+    untimed) until the budget is spent, and the mean is reported."""
     import numpy as np
     import oracle
 
@@ -146,21 +178,38 @@ def cpu_baseline(w, x0, plan, traffic_bytes, budget_s=10.0):
         else:
             sched = oracle.Schedule(w.p, w.bandwidths, w.n, w.k, seg_lo=0, seg_hi=nseg)
         t = time.perf_counter()
-        oracle.run(sched, w.dtype, host)
+        if threads == 1:
+            oracle.run(sched, w.dtype, host)
+        else:
+            oracle.run_parallel(sched, w.dtype, host, threads)
         return time.perf_counter() - t, end
 
-    t1, _ = run(1)
-    nseg = int(max(1, min(total, budget_s / max(t1, 1e-6))))
+    first = min(total, threads)  # at least one segment per thread
+    t1, _ = run(first)
+    nseg = int(max(first, min(total, first * budget_s / max(t1, 1e-6))))
     times = []
     while not times or (nseg == total and sum(times) < budget_s and len(times) < 20):
         t, elems = run(nseg)
         times.append(t)
     t = sum(times) / len(times)
     bytes_sample = traffic_bytes * elems / w.n
-    return {"value": round(bytes_sample / t / 1e9, 4), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
+    how = "serial C oracle" if threads == 1 else f"the oracle's steps on {threads} OpenMP threads"
+    return {"value": round(bytes_sample / t / 1e9, 4), "unit": "GB/s", "cores": threads,
             "sample": f"first {nseg} of {total} segments ({elems} of {w.n} elements per rank), "
-                      f"serial C oracle, mean of {len(times)} run(s) of {t:.2f} s"}
+                      f"{how}, mean of {len(times)} run(s) of {t:.3f} s"}
+
+
+def cpu_baseline(w, x0, plan, traffic_bytes, serial_s, parallel_s):
+    """Two legs: the serial oracle on one core, and the same executor on all
+    the cores this process may use."""
+    serial = cpu_leg(w, x0, plan, traffic_bytes, serial_s, 1)
+    threads = oracle_threads()
+    par = cpu_leg(w, x0, plan, traffic_bytes, parallel_s, threads)
+    out = dict(serial)
+    out["kind"] = "oracle"
+    out["all_cores"] = dict(par, kind="oracle, OpenMP over segments (bit-identical to serial)")
+    out.update(host_info())
+    return out
 
 
 def copy_rate(torch, nbytes, steps, warmup):
@@ -189,49 +238,54 @@ def copy_bench(torch, args):
                       "GBps_read_plus_write": round(gbps, 2)}), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="p8_f32")
-    ap.add_argument("--launches", type=int, default=1, choices=[0, 1],
-                    help="1: fused (default); 0: one launch per stage slot")
-    ap.add_argument("--stages", action="store_true",
-                    help="also time every stage slot on its own (per-stage breakdown)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-check", action="store_true")
-    ap.add_argument("--copy-only", action="store_true",
-                    help="time torch's plain device-to-device copy instead (the reference "
-                         "kernel for scaling rocprofv3 byte counters)")
-    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
-    ap.add_argument("--n", type=int, default=None,
-                    help="elements per rank instead of the workload's own N (message-size "
-                         "sweeps); the line then reports that N and no counter traffic")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: the OptCC emulation runs the p logical ranks on ONE GPU; "
-              "it takes --gpus 1 only.", file=sys.stderr)
-        sys.exit(2)
+BASELINE_CONFIGS = ["p4_f32", "p8_f32", "p8_i32", "p16_bf16", "p64_f32", "p128_f32"]
 
-    import torch
-    from paper_2606_01680_amd import optcc
-    from paper_2606_01680_amd.workloads import ESIZE, WORKLOADS, make_inputs
 
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        sys.exit(1)
-    torch.cuda.set_device(0)
-    if args.copy_only:
-        copy_bench(torch, args)
-        return
-    w = WORKLOADS[args.workload]
-    if args.n is not None:
-        import dataclasses
-        if args.n < 1:
-            print("bench.py: --n must be >= 1", file=sys.stderr)
-            sys.exit(2)
-        w = dataclasses.replace(w, n=args.n)
+def full_check(torch, w, x, x0):
+    """Properties at full size: all ranks bitwise identical, and every element
+    within the error bound of the exact sum (exactly the wrapped sum for
+    int32).  x holds the result of one AllReduce of x0."""
+    iv = x.view(torch.int16) if x.element_size() == 2 else x.view(torch.int32)
+    ok = all(torch.equal(iv[r], iv[0]) for r in range(1, w.p))
+    chunk = max(1 << 16, (1 << 28) // w.p)
+    for c0 in range(0, w.n, chunk):
+        c1 = min(w.n, c0 + chunk)
+        if w.dtype == "i32":
+            want = x0[:, c0:c1].to(torch.int64).sum(0)
+            ok &= torch.equal(x[0, c0:c1], ((want + 2**31) % 2**32 - 2**31).to(torch.int32))
+        else:
+            xs = x0[:, c0:c1].to(torch.float64)
+            u = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}[w.dtype]
+            err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
+            ok &= bool((err <= w.p * u * xs.abs().sum(0)).all())
+    return "pass" if ok else "FAIL"
+
+
+def model_times(optcc, w, plan):
+    """Model times of the paper's bandwidth model, in units of N element-times."""
+    n = w.n
+    t_model = optcc.optcc_model_time(plan) / n
+    if w.g > 1:
+        lb = optcc.optcc_lower_bound_servers(w.q, w.g, w.bandwidths, n) / n
+    else:
+        lb = optcc.optcc_lower_bound(w.p, w.bandwidths, n) / n
+    t0_ring = 2.0 * (w.p - 1) / (w.g * w.p)  # fault-free optimum with g GPUs per server
+    # the same flows timed in the paper's network model (list scheduling)
+    evaluated = None
+    if plan.num_flows <= (1 << 20):
+        evaluated = round(plan.timeline(with_flows=False)[0] / n, 6)
+    return {"optcc": round(t_model, 6), "evaluated_schedule": evaluated,
+            "fault_free_ring_T0": round(t0_ring, 6), "lower_bound": round(lb, 6),
+            "degraded_ring": round(float(max(plan.slowdowns)) * t0_ring, 6)}
+
+
+def measure(torch, optcc, w, args, check=True):
+    """Time args.steps back-to-back AllReduces of workload w (after
+    args.warmup untimed ones), HIP events around each launch, then check
+    one more at full size.  Returns the record and what the CPU baseline
+    needs; `launches` counts the executor's kernel launches issued."""
+    from paper_2606_01680_amd.workloads import make_inputs
+
     x = make_inputs(w, device="cuda:0")
     x0 = x.clone()
     if w.g > 1:  # q servers of g GPUs (App. E)
@@ -241,6 +295,7 @@ def main():
     nslots = plan.num_slots
     rd, wr = plan.traffic(w.dtype, 0, nslots, args.launches)
     alg_bytes = rd + wr
+    per_call = 1 if args.launches == 1 else nslots
 
     def step():
         optcc.optcc_allreduce_emulate_slots(x, w.p, w.n, w.dtype, plan, 0, nslots, args.launches)
@@ -261,68 +316,35 @@ def main():
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms_total = t0.elapsed_time(t1)
-    ms_step = ms_total / args.steps
+    ms_step = t0.elapsed_time(t1) / args.steps
     launch_ms = [a.elapsed_time(b) for a, b in evs]
     ms_launch = sum(launch_ms) / len(launch_ms)
+    launches = (args.warmup + args.steps) * per_call
 
-    stages = stage_breakdown(torch, optcc, x, w, plan, args.steps, args.warmup) if args.stages \
-        else None
+    stages = None
+    if args.stages:
+        stages = stage_breakdown(torch, optcc, x, w, plan, args.steps, args.warmup)
+        launches += len(stages) * (args.steps + args.warmup)
 
-    check = "skipped"
-    if not args.no_check:  # the timed path computes the sum: properties at full size
+    result = "skipped"
+    if check:  # the timed path computes the sum: properties at full size
         x.copy_(x0)
         step()
         torch.cuda.synchronize()
-        iv = x.view(torch.int16) if x.element_size() == 2 else x.view(torch.int32)
-        ok = all(torch.equal(iv[r], iv[0]) for r in range(1, w.p))
-        chunk = max(1 << 16, (1 << 28) // w.p)
-        for c0 in range(0, w.n, chunk):
-            c1 = min(w.n, c0 + chunk)
-            if w.dtype == "i32":
-                want = x0[:, c0:c1].to(torch.int64).sum(0)
-                ok &= torch.equal(x[0, c0:c1], ((want + 2**31) % 2**32 - 2**31).to(torch.int32))
-            else:
-                xs = x0[:, c0:c1].to(torch.float64)
-                u = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}[w.dtype]
-                err = (x[0, c0:c1].to(torch.float64) - xs.sum(0)).abs()
-                ok &= bool((err <= w.p * u * xs.abs().sum(0)).all())
-        check = "pass" if ok else "FAIL"
+        launches += per_call
+        result = full_check(torch, w, x, x0)
+    del x
 
     achieved = alg_bytes / (ms_launch * 1e-3) / 1e9
     # counter traffic was taken at the workload's own N
     traffic = measured_traffic(w.name, args.launches) if args.n is None else None
-    n = w.n
-    t_model = optcc.optcc_model_time(plan) / n
-    if w.g > 1:
-        lb = optcc.optcc_lower_bound_servers(w.q, w.g, w.bandwidths, n) / n
-    else:
-        lb = optcc.optcc_lower_bound(w.p, w.bandwidths, n) / n
-    t0_ring = 2.0 * (w.p - 1) / (w.g * w.p)  # fault-free optimum with g GPUs per server
-    # the same flows timed in the paper's network model (list scheduling)
-    evaluated = None
-    if plan.num_flows <= (1 << 20):
-        evaluated = round(plan.timeline(with_flows=False)[0] / n, 6)
-    out = {
-        "metric": METRIC,
-        "value": round(alg_bytes / (ms_step * 1e-3) / 1e9, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+    rec = {
+        "workload": w.name, "p": w.p, "N": w.n, "n_chunks": w.k, "dtype": w.dtype,
+        "gpus_per_server": w.g,
+        "stragglers": {str(int(r)): float(w.bandwidths[int(r)]) for r in plan.stragglers},
+        "values": w.values, "plan_kind": plan.kind, "launches_per_step": per_call,
         "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": w.dtype,
-        "data": "synthetic",
-        "config": {
-            "workload": w.name, "p": w.p, "N": w.n, "n_chunks": w.k,
-            "gpus_per_server": w.g,
-            "stragglers": {str(int(r)): float(w.bandwidths[int(r)]) for r in plan.stragglers},
-            "values": w.values, "launches_per_step": 1 if args.launches == 1 else nslots,
-            "plan_kind": plan.kind,
-        },
+        "GBps": round(alg_bytes / (ms_step * 1e-3) / 1e9, 2),
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
@@ -334,26 +356,190 @@ def main():
             "kernel_ms_median": round(statistics.median(launch_ms), 5),
             "kernel_ms_min": round(min(launch_ms), 5), "kernel": "optcc_exec_kernel",
         },
-        "model_time_over_N": {"optcc": round(t_model, 6), "evaluated_schedule": evaluated,
-                              "fault_free_ring_T0": round(t0_ring, 6),
-                              "lower_bound": round(lb, 6),
-                              "degraded_ring": round(float(max(plan.slowdowns)) * t0_ring, 6)},
+        "model_time_over_N": model_times(optcc, w, plan),
+        "check": result,
+        "wall_s_timed": round(wall, 4),
+        "executor_launches": launches,
+    }
+    if stages is not None:
+        rec["stages"] = stages
+    return rec, x0, plan, alg_bytes
+
+
+def trace_summary(csv_path, line_path):
+    """Split a rocprofv3 kernel trace of one bench run by workload: the
+    executor's dispatches, in dispatch order, belong to the workloads in the
+    order the bench line lists them (dispatch_order), so each workload's
+    average kernel duration can be set beside its line figures."""
+    import csv
+
+    line = None
+    for text in open(line_path):
+        text = text.strip()
+        if text.startswith("{") and '"metric"' in text:
+            line = json.loads(text)
+    if line is None:
+        raise SystemExit(f"no bench line in {line_path}")
+    rows = []
+    with open(csv_path, newline="") as f:
+        for r in csv.DictReader(f):
+            if "optcc_exec_kernel" in r["Kernel_Name"]:
+                rows.append((int(r["Dispatch_Id"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"]),
+                             r["Kernel_Name"]))
+    rows.sort()
+    order = line["dispatch_order"]
+    if sum(n for _, n in order) != len(rows):
+        raise SystemExit(f"trace has {len(rows)} executor dispatches, the line lists "
+                         f"{sum(n for _, n in order)}")
+    recs = dict(line.get("configs", {}))
+    recs.setdefault(line["config"]["workload"], {"roofline": line["roofline"]})
+    print("| Workload | Kernel | Dispatches | Avg ns | Min ns | Max ns | bench kernel_ms | "
+          "alg. GB/s at the trace average | frac |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    at = 0
+    for name, n in order:
+        part = rows[at:at + n]
+        at += n
+        ns = [d for _, d, _ in part]
+        names = sorted(set(k for _, _, k in part))
+        roof = recs[name]["roofline"]
+        avg = sum(ns) / len(ns)
+        rate = roof["algorithmic_bytes"] / avg
+        print(f"| {name} | {' / '.join(names)} | {n} | {avg:,.0f} | {min(ns):,} | {max(ns):,} | "
+              f"{roof['kernel_ms']} | {rate:,.1f} | {rate / PEAK_GBPS:.4f} |")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=None,
+                    help="one workload only (default: the p8_f32 headline plus every "
+                         "headline configuration under \"configs\")")
+    ap.add_argument("--launches", type=int, default=1, choices=[0, 1],
+                    help="1: fused (default); 0: one launch per stage slot")
+    ap.add_argument("--stages", action="store_true",
+                    help="also time every stage slot on its own (per-stage breakdown)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="measure the headline (or --workload) only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="budget of the headline's serial oracle leg (the all-cores leg gets "
+                         "half, every other configuration a fifth per leg)")
+    ap.add_argument("--copy-only", action="store_true",
+                    help="time torch's plain device-to-device copy instead (the reference "
+                         "kernel for scaling rocprofv3 byte counters)")
+    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--n", type=int, default=None,
+                    help="elements per rank instead of the workload's own N (message-size "
+                         "sweeps); the line then reports that N and no counter traffic")
+    ap.add_argument("--trace-summary", metavar="CSV", default=None,
+                    help="split a rocprofv3 kernel trace of a bench run by workload (no GPU)")
+    ap.add_argument("--line", metavar="FILE", default=None,
+                    help="the bench run's output, holding its JSON line (with --trace-summary)")
+    args = ap.parse_args()
+    if args.trace_summary:
+        if not args.line:
+            ap.error("--trace-summary needs --line")
+        trace_summary(args.trace_summary, args.line)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: the OptCC emulation runs the p logical ranks on ONE GPU; "
+              "it takes --gpus 1 only.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_01680_amd import optcc
+    from paper_2606_01680_amd.workloads import ESIZE, WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.copy_only:
+        copy_bench(torch, args)
+        return
+    sweep = args.workload is None and args.n is None and not args.no_configs
+    w = WORKLOADS[args.workload or "p8_f32"]
+    if args.n is not None:
+        import dataclasses
+        if args.n < 1:
+            print("bench.py: --n must be >= 1", file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, n=args.n)
+
+    rec, x0, plan, alg_bytes = measure(torch, optcc, w, args, check=not args.no_check)
+    order = [[w.name, rec["executor_launches"]]]
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, x0, plan, alg_bytes, args.cpu_seconds, args.cpu_seconds / 2)
+    del x0
+    torch.cuda.empty_cache()
+    n = w.n
+    times = rec["model_time_over_N"]
+    out = {
+        "metric": METRIC,
+        "value": rec["GBps"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": rec["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "p": w.p, "N": w.n, "n_chunks": w.k,
+            "gpus_per_server": w.g, "stragglers": rec["stragglers"], "values": w.values,
+            "launches_per_step": rec["launches_per_step"], "plan_kind": plan.kind,
+        },
+        "roofline": rec["roofline"],
+        "model_time_over_N": times,
         # the same model times in seconds for this message on healthy
         # 200 Gb/s NICs (25 GB/s, the paper's ConnectX-6 HDR setting)
         "model_seconds_at_25GBps_nic": {
-            k: round(v * n * ESIZE[w.dtype] / NIC_BYTES_PER_S, 6)
-            for k, v in (("optcc", t_model), ("fault_free_ring_T0", t0_ring),
-                         ("lower_bound", lb))},
-        "check": check,
+            k: round(times[key] * n * ESIZE[w.dtype] / NIC_BYTES_PER_S, 6)
+            for k, key in (("optcc", "optcc"), ("fault_free_ring_T0", "fault_free_ring_T0"),
+                           ("lower_bound", "lower_bound"))},
+        "check": rec["check"],
         "kernel_sha256_16": kernel_hash(),
-        "wall_s_timed": round(wall, 4),
+        "wall_s_timed": rec["wall_s_timed"],
     }
-    if stages is not None:
-        out["stages"] = stages
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, x0, plan, alg_bytes)
+    if "stages" in rec:
+        out["stages"] = rec["stages"]
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    failed = rec["check"] == "FAIL"
+    if sweep:
+        configs = {}
+        for name in BASELINE_CONFIGS:
+            if name == w.name:
+                r = {k: v for k, v in rec.items() if k not in ("executor_launches", "stages")}
+                if cpu is not None:
+                    r["cpu_baseline"] = {"serial": {k: cpu[k] for k in ("value", "cores", "sample")},
+                                         "all_cores": cpu["all_cores"]}
+                configs[name] = r
+                continue
+            print(f"bench: measuring {name}", file=sys.stderr, flush=True)
+            wc = WORKLOADS[name]
+            r, xc, pc, bc = measure(torch, optcc, wc, args, check=not args.no_check)
+            order.append([name, r.pop("executor_launches")])
+            if not args.no_cpu_baseline:
+                legs = args.cpu_seconds / 5
+                r["cpu_baseline"] = {"serial": cpu_leg(wc, xc, pc, bc, legs, 1),
+                                     "all_cores": cpu_leg(wc, xc, pc, bc, legs, oracle_threads())}
+            del xc
+            torch.cuda.empty_cache()
+            failed |= r["check"] == "FAIL"
+            configs[name] = r
+        out["configs"] = configs
+    out["dispatch_order"] = order
     print(json.dumps(out), flush=True)
-    if check == "FAIL":
+    if failed:
         sys.exit(3)
 
 

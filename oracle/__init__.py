@@ -7,7 +7,7 @@ nothing from the product.
 
 Parts (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
 
-* ``Schedule`` / ``run`` / ``run_sampled``: the schedule built from the rules
+* ``Schedule`` / ``run`` / ``run_parallel`` / ``run_sampled``: the schedule built from the rules
   of Sec. 4.1-4.2, App. C (bubble filling) and App. D (several stragglers),
   executed serially step by step in plain C (``optcc_oracle.c``).
 * ``brute_sum``: the definition of the result (Sec. 3, problem setting): the
@@ -45,7 +45,7 @@ _lib = None
 
 def build_lib() -> str:
     """Compile the oracle with plain gcc: no fast-math, no contraction."""
-    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
+    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
            "-shared", "-fPIC", "-o", _LIB + ".tmp", _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(_LIB + ".tmp", _LIB)
@@ -69,6 +69,8 @@ def lib():
         L.orc_steps.argtypes = [vp, vp, vp, vp]
         L.orc_run.argtypes = [vp, i32, vp, i32, i32]
         L.orc_run.restype = i32
+        L.orc_run_parallel.argtypes = [vp, i32, vp, i32, i32, i32]
+        L.orc_run_parallel.restype = i32
         L.orc_run_sampled.argtypes = [vp, i32, vp, vp, i64, i32, i32]
         L.orc_run_sampled.restype = i32
         L.orc_last_error.restype = ctypes.c_char_p
@@ -174,6 +176,21 @@ def run(sched: Schedule, dtype: str, bufs: np.ndarray, slot_lo=0, slot_hi=NUM_SE
         raise ValueError("bufs must be a C-contiguous [p, N] array of the dtype")
     ptrs = (ctypes.c_void_p * sched.p)(*[bufs[r].ctypes.data for r in range(sched.p)])
     rc = sched._L.orc_run(sched._h, DTYPES[dtype], ptrs, int(slot_lo), int(slot_hi))
+    if rc != 0:
+        raise OracleError(rc, sched._L.orc_last_error().decode())
+    return bufs
+
+
+def run_parallel(sched: Schedule, dtype: str, bufs: np.ndarray, threads: int,
+                 slot_lo=0, slot_hi=NUM_SERVER_SLOTS):
+    """``run`` on `threads` host threads (OpenMP over segments): the same
+    bits as the serial execution, used to time the oracle on all cores."""
+    if not (bufs.flags.c_contiguous and bufs.shape == (sched.p, sched.n)
+            and bufs.dtype == NP_DTYPES[dtype]):
+        raise ValueError("bufs must be a C-contiguous [p, N] array of the dtype")
+    ptrs = (ctypes.c_void_p * sched.p)(*[bufs[r].ctypes.data for r in range(sched.p)])
+    rc = sched._L.orc_run_parallel(sched._h, DTYPES[dtype], ptrs, int(slot_lo), int(slot_hi),
+                                   int(threads))
     if rc != 0:
         raise OracleError(rc, sched._L.orc_last_error().decode())
     return bufs

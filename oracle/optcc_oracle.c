@@ -19,6 +19,10 @@
  *     after Stage 4 (read literally the printed text is not an AllReduce);
  *   - one rounding per step; sizes in whole quanta of 64 elements.
  *
+ * orc_run executes the steps serially; orc_run_parallel gives the same bits
+ * on several host threads (OpenMP over segments, each segment's steps in
+ * serial order), for timing the oracle on all host cores.
+ *
  * Pins (tests outside this file): exact int32 sums against the definition of
  * the result; contributor sets (nobody counted twice, everybody counted);
  * the fp error bound of recursive summation; a chain's association order
@@ -673,6 +677,42 @@ int orc_run(const orc_sched *s, int dtype, void **bufs, int slot_lo, int slot_hi
     const int32_t *srcs = s->srcpool + st->src_at;
     for (int64_t c = st->off; c < st->off + st->len; ++c) apply_elem(dtype, st, srcs, bufs, c);
   }
+  return 0;
+}
+
+/* Same result as orc_run, bit for bit, on `nthreads` host threads (OpenMP).
+ * Every step reads and writes coordinates of its own segment only, and a
+ * coordinate's steps run in serial order whatever the thread: the segments
+ * are shared out among the threads, and each runs its segment's steps in
+ * the serial order of orc_run.  So every coordinate sees exactly the
+ * operations of orc_run, in the same order. */
+int orc_run_parallel(const orc_sched *s, int dtype, void **bufs, int slot_lo, int slot_hi,
+                     int nthreads) {
+  if (dtype < 0 || dtype > 3) { g_err = "bad dtype"; return -1; }
+  if (nthreads < 1) { g_err = "nthreads must be >= 1"; return -1; }
+  int nseg = s->nseg;
+  /* step indices grouped by segment, each group in serial order */
+  int64_t *start = (int64_t *)calloc((size_t)nseg + 1, sizeof(int64_t));
+  int64_t *order = (int64_t *)malloc((size_t)(s->nsteps ? s->nsteps : 1) * sizeof(int64_t));
+  if (!start || !order) { free(start); free(order); g_err = "out of memory"; return -2; }
+  for (int64_t i = 0; i < s->nsteps; ++i) start[s->steps[i].seg + 1]++;
+  for (int g = 0; g < nseg; ++g) start[g + 1] += start[g];
+  int64_t *fill = (int64_t *)malloc(((size_t)nseg + 1) * sizeof(int64_t));
+  if (!fill) { free(start); free(order); g_err = "out of memory"; return -2; }
+  memcpy(fill, start, ((size_t)nseg + 1) * sizeof(int64_t));
+  for (int64_t i = 0; i < s->nsteps; ++i) order[fill[s->steps[i].seg]++] = i;
+  free(fill);
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+  for (int g = 0; g < nseg; ++g) {
+    for (int64_t a = start[g]; a < start[g + 1]; ++a) {
+      const orc_step *st = &s->steps[order[a]];
+      if (st->slot < slot_lo || st->slot >= slot_hi) continue;
+      const int32_t *srcs = s->srcpool + st->src_at;
+      for (int64_t c = st->off; c < st->off + st->len; ++c) apply_elem(dtype, st, srcs, bufs, c);
+    }
+  }
+  free(start);
+  free(order);
   return 0;
 }
 
