@@ -193,6 +193,28 @@ int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N, optcc_dty
                                   int launches, void *stream);
 
 /*
+ * optcc_allreduce_emulate_noalloc - optcc_allreduce_emulate for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, result (bit for
+ * bit) and errors as optcc_allreduce_emulate, and the caller still passes the
+ * buffers.  It calls no hipMalloc, hipFree or other allocating routine: the
+ * plan's step tables (32 bytes per segment, rounded up to 256, plus 16 bytes
+ * per tile of 1024-8192 elements) are copied on `stream`, on every call, into
+ * a static device array of OPTCC_NOALLOC_SCRATCH_BYTES that the library holds
+ * on each GPU it runs on until the process ends; a plan whose tables need
+ * more is refused with OPTCC_EUNSUPPORTED before any device call (about 2^29
+ * elements per rank at 2048-element tiles fit).  Every call on one GPU shares
+ * that GPU's array, which keeps the last call's tables (nothing in it must
+ * start at zero): calls on one GPU that overlap in time (on different
+ * streams, or from several host threads without ordering) race and give
+ * undefined results.  The plan must stay alive until the call's work on
+ * `stream` has completed (its host tables are the copies' source).
+ */
+#define OPTCC_NOALLOC_SCRATCH_BYTES (4 << 20)
+int optcc_allreduce_emulate_noalloc(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
+                                    const optcc_plan_t *plan, void *stream);
+
+/*
  * optcc_model_time - completion time of the plan's schedule in the paper's
  * bandwidth-bound model (a healthy NIC moves one element per time unit; Sec. 3),
  * for N elements per rank, in fp64:

@@ -23,6 +23,30 @@ using namespace kern;
 // uploaded on first use and cached.  The upload (hipMalloc, hipMemcpy) may
 // not run while `stream` is being captured into a graph: such a first call
 // fails before touching the device, and the capture stays valid.
+// The plan's host tile table for tiles of tile_elems elements: tile_elems-
+// element pieces of every segment's ring part and P2P chunk, built once per
+// tile length.  The caller holds pl.mu; the vector lives as long as the plan.
+const std::vector<TileDesc> &host_tiles(const optcc_plan_t &pl, int tile_elems) {
+  auto it = pl.host_tiles.find(tile_elems);
+  if (it != pl.host_tiles.end()) return it->second;
+  std::vector<TileDesc> &tiles = pl.host_tiles[tile_elems];
+  for (int g = 0; g < pl.nseg; ++g) {
+    const Segment &s = pl.seg[(size_t)g];
+    auto cut = [&](int64_t b, int64_t e, int is_p2p) {
+      for (int64_t x = b; x < e; x += tile_elems) {
+        TileDesc t;
+        t.begin = x;
+        t.len = (int32_t)std::min<int64_t>(tile_elems, e - x);
+        t.meta = (g << 1) | is_p2p;
+        tiles.push_back(t);
+      }
+    };
+    cut(std::min(s.ring_begin, pl.n), s.ring_end, 0);
+    cut(s.p2p_begin, s.p2p_end, 1);
+  }
+  return tiles;
+}
+
 int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
@@ -38,22 +62,7 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, De
     return fail(OPTCC_EINVAL,
                 "the stream is being captured and this plan's tables for this device and "
                 "element size are not uploaded yet: run the plan once outside the capture first");
-  // Tiles: tile_elems-element pieces of every segment's ring part and P2P chunk.
-  std::vector<TileDesc> tiles;
-  for (int g = 0; g < pl.nseg; ++g) {
-    const Segment &s = pl.seg[(size_t)g];
-    auto cut = [&](int64_t b, int64_t e, int is_p2p) {
-      for (int64_t x = b; x < e; x += tile_elems) {
-        TileDesc t;
-        t.begin = x;
-        t.len = (int32_t)std::min<int64_t>(tile_elems, e - x);
-        t.meta = (g << 1) | is_p2p;
-        tiles.push_back(t);
-      }
-    };
-    cut(std::min(s.ring_begin, pl.n), s.ring_end, 0);
-    cut(s.p2p_begin, s.p2p_end, 1);
-  }
+  const std::vector<TileDesc> &tiles = host_tiles(pl, tile_elems);
   DeviceTables d;
   const size_t sb = pl.segdesc.size() * sizeof(SegDesc);
   const size_t tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
@@ -71,6 +80,63 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, De
   d.ntiles = (int64_t)tiles.size();
   pl.dev[{dev, tile_elems}] = d;
   *out = d;
+  return OPTCC_OK;
+}
+
+// Device memory of optcc_allreduce_emulate_noalloc: the plan's tables are
+// staged here on every call instead of in memory of their own.  One copy per
+// GPU, held until the process ends; calls on one GPU share it.
+static __device__ __align__(256) unsigned char scratch[OPTCC_NOALLOC_SCRATCH_BYTES];
+
+// Device address of this GPU's `scratch` (the array's name is a host-side
+// stand-in in host code): looked up once per device, with it current.
+int scratch_address(void **out) {
+  static std::mutex mu;
+  static std::map<int, void *> addr;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return fail(OPTCC_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(err));
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void *ptr = nullptr;
+    err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || !ptr)
+      return fail(OPTCC_EDEVICE, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(err));
+    it = addr.emplace(dev, ptr).first;
+  }
+  *out = it->second;
+  return OPTCC_OK;
+}
+
+// The plan's tables staged in `scratch` by two copies on `stream` (no device
+// allocation).  The host tables are the plan's and live as long as it does.
+int scratch_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
+  const std::vector<TileDesc> *tiles;
+  {
+    std::lock_guard<std::mutex> lk(pl.mu);
+    tiles = &host_tiles(pl, tile_elems);
+  }
+  const size_t seg_bytes = pl.segdesc.size() * sizeof(SegDesc);
+  const size_t tile_off = (seg_bytes + 255) / 256 * 256;
+  const size_t tile_bytes = tiles->size() * sizeof(TileDesc);
+  if (tile_off + tile_bytes > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
+    return fail(OPTCC_EUNSUPPORTED,
+                "the plan's tables need " + std::to_string(tile_off + tile_bytes) +
+                    " bytes, more than the " + std::to_string(OPTCC_NOALLOC_SCRATCH_BYTES) +
+                    " of the no-allocation scratch array: use optcc_allreduce_emulate");
+  void *base = nullptr;
+  int rc = scratch_address(&base);
+  if (rc != OPTCC_OK) return rc;
+  char *b = static_cast<char *>(base);
+  hipError_t err = hipMemcpyAsync(b, pl.segdesc.data(), seg_bytes, hipMemcpyHostToDevice, stream);
+  if (err == hipSuccess && tile_bytes)
+    err = hipMemcpyAsync(b + tile_off, tiles->data(), tile_bytes, hipMemcpyHostToDevice, stream);
+  if (err != hipSuccess)
+    return fail(OPTCC_EDEVICE, std::string("staging plan tables: ") + hipGetErrorString(err));
+  out->segs = reinterpret_cast<SegDesc *>(b);
+  out->tiles = reinterpret_cast<TileDesc *>(b + tile_off);
+  out->ntiles = (int64_t)tiles->size();
   return OPTCC_OK;
 }
 
@@ -105,7 +171,7 @@ int one_workgroup_per_cu_lds() {
 }
 
 int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optcc_plan_t *pl,
-            int sb, int se, int launches, void *stream) {
+            int sb, int se, int launches, void *stream, bool noalloc = false) {
   set_error("");
   if (!pl) return fail(OPTCC_EINVAL, "plan is NULL");
   if (!bufs) return fail(OPTCC_EINVAL, "bufs is NULL");
@@ -163,7 +229,8 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   const int vec_tile = kern::kThreads * (int)(16 / es);
   while (tile_elems > vec_tile && N / tile_elems < kTileMinCount) tile_elems /= 2;
   DeviceTables dt;
-  int rc = device_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt);
+  int rc = noalloc ? scratch_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt)
+                   : device_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt);
   if (rc != OPTCC_OK) return rc;
   KArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -239,6 +306,13 @@ extern "C" int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N
                                              int slot_begin, int slot_end, int launches,
                                              void *stream) {
   return emulate(bufs, p, N, dtype, plan, slot_begin, slot_end, launches, stream);
+}
+
+extern "C" int optcc_allreduce_emulate_noalloc(void *const *bufs, int p, int64_t N,
+                                               optcc_dtype_t dtype, const optcc_plan_t *plan,
+                                               void *stream) {
+  return emulate(bufs, p, N, dtype, plan, 0, plan ? plan->nslots : OPTCC_NUM_SLOTS, 1, stream,
+                 true);
 }
 
 extern "C" void optcc_plan_free(optcc_plan_t *pl) {

@@ -82,6 +82,8 @@ struct optcc_plan {
   // device copies of segdesc/tiles, per (device ordinal, tile length)
   mutable std::mutex mu;
   mutable std::map<std::pair<int, int>, optcc::DeviceTables> dev;  // (device, tile elements)
+  // host tile tables per tile length (the source of the device copies)
+  mutable std::map<int, std::vector<optcc::TileDesc>> host_tiles;
 };
 
 namespace optcc {

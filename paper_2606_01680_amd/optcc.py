@@ -25,7 +25,8 @@ DTYPES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3}
 KINDS = {0: "ring", 1: "single_ge2", 2: "single_lt2", 3: "multi", 4: "servers"}
 
 EXPORTED = ("optcc_plan", "optcc_plan_servers", "optcc_plan_free", "optcc_allreduce_emulate",
-            "optcc_allreduce_emulate_slots", "optcc_model_time", "optcc_lower_bound",
+            "optcc_allreduce_emulate_slots", "optcc_allreduce_emulate_noalloc",
+            "optcc_model_time", "optcc_lower_bound",
             "optcc_lower_bound_servers", "optcc_last_error", "optcc_plan_info",
             "optcc_plan_segments", "optcc_plan_num_flows", "optcc_plan_get_flows",
             "optcc_plan_traffic", "optcc_plan_timeline", "optcc_narrow_f32")
@@ -79,6 +80,8 @@ def _load():
     L.optcc_allreduce_emulate.restype = i32
     L.optcc_allreduce_emulate_slots.argtypes = [vp, i32, i64, i32, vp, i32, i32, i32, vp]
     L.optcc_allreduce_emulate_slots.restype = i32
+    L.optcc_allreduce_emulate_noalloc.argtypes = [vp, i32, i64, i32, vp, vp]
+    L.optcc_allreduce_emulate_noalloc.restype = i32
     L.optcc_model_time.argtypes = [vp, vp]
     L.optcc_model_time.restype = dbl
     L.optcc_lower_bound.argtypes = [i32, vp, i64]
@@ -303,6 +306,18 @@ def optcc_allreduce_emulate(bufs, p: int, N: int, dtype: str, plan: Plan, stream
     st = _stream(stream)
     _check(_lib.optcc_allreduce_emulate(arr, int(p), int(N), DTYPES[dtype], plan.handle,
                                         ctypes.c_void_p(st)))
+    _keep_if_captured(plan, st)
+
+
+def optcc_allreduce_emulate_noalloc(bufs, p: int, N: int, dtype: str, plan: Plan,
+                                    stream=None) -> None:
+    """optcc_allreduce_emulate without any device allocation: the plan's
+    tables are staged in the library's static per-GPU array on `stream`
+    (calls on one GPU that overlap in time race)."""
+    arr = _ptr_array(bufs, p, int(N), dtype)
+    st = _stream(stream)
+    _check(_lib.optcc_allreduce_emulate_noalloc(arr, int(p), int(N), DTYPES[dtype], plan.handle,
+                                                ctypes.c_void_p(st)))
     _keep_if_captured(plan, st)
 
 

@@ -308,3 +308,19 @@ def test_segment_quanta_beyond_32_bits_refused(o):
         ptrs = (ctypes.c_void_p * p)(*[(r + 1) << 45 for r in range(p)])
         rc = L.optcc_allreduce_emulate(ptrs, p, n, 2, pl.handle, None)
         assert rc == o.OPTCC_EUNSUPPORTED and "quanta" in o.optcc_last_error()
+
+
+def test_noalloc_refuses_tables_beyond_its_scratch(o):
+    """optcc_allreduce_emulate_noalloc stages the plan's tables in a static
+    array of OPTCC_NOALLOC_SCRATCH_BYTES: a plan whose tables need more is
+    refused with OPTCC_EUNSUPPORTED before any device call (the pointers are
+    never dereferenced)."""
+    L = o.lib()
+    n = 1 << 30  # p = 3 fp32 takes 4096-element tiles: 2^18 tiles of 16 bytes = 4 MiB
+    pl = o.optcc_plan(3, [1.0] * 3, n, 4)
+    ptrs = (ctypes.c_void_p * 3)(*[(r + 1) << 40 for r in range(3)])
+    rc = L.optcc_allreduce_emulate_noalloc(ptrs, 3, n, 0, pl.handle, None)
+    assert rc == o.OPTCC_EUNSUPPORTED
+    assert "scratch" in o.optcc_last_error()
+    # the argument checks of optcc_allreduce_emulate apply as well
+    assert L.optcc_allreduce_emulate_noalloc(ptrs, 4, n, 0, pl.handle, None) == o.OPTCC_EINVAL
