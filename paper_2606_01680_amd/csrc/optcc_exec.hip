@@ -9,6 +9,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "optcc_internal.hpp"
@@ -45,6 +46,18 @@ const std::vector<TileDesc> &host_tiles(const optcc_plan_t &pl, int tile_elems) 
     cut(s.p2p_begin, s.p2p_end, 1);
   }
   return tiles;
+}
+
+// Number of tiles host_tiles cuts for tiles of tile_elems elements.
+int64_t tile_count(const optcc_plan_t &pl, int tile_elems) {
+  int64_t t = 0;
+  for (int g = 0; g < pl.nseg; ++g) {
+    const Segment &s = pl.seg[(size_t)g];
+    const int64_t rb = std::min(s.ring_begin, pl.n);
+    if (s.ring_end > rb) t += (s.ring_end - rb + tile_elems - 1) / tile_elems;
+    if (s.p2p_end > s.p2p_begin) t += (s.p2p_end - s.p2p_begin + tile_elems - 1) / tile_elems;
+  }
+  return t;
 }
 
 int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
@@ -109,6 +122,13 @@ int scratch_address(void **out) {
   return OPTCC_OK;
 }
 
+// Bytes of the plan's tables for `ntiles` tiles staged in the no-allocation
+// array: segment descriptors (rounded up to 256 bytes), then the tiles.
+size_t scratch_bytes(const optcc_plan_t &pl, int64_t ntiles) {
+  const size_t seg_bytes = pl.segdesc.size() * sizeof(SegDesc);
+  return (seg_bytes + 255) / 256 * 256 + (size_t)ntiles * sizeof(TileDesc);
+}
+
 // The plan's tables staged in `scratch` by two copies on `stream` (no device
 // allocation).  The host tables are the plan's and live as long as it does.
 int scratch_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
@@ -120,7 +140,7 @@ int scratch_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, D
   const size_t seg_bytes = pl.segdesc.size() * sizeof(SegDesc);
   const size_t tile_off = (seg_bytes + 255) / 256 * 256;
   const size_t tile_bytes = tiles->size() * sizeof(TileDesc);
-  if (tile_off + tile_bytes > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
+  if (scratch_bytes(pl, (int64_t)tiles->size()) > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
     return fail(OPTCC_EUNSUPPORTED,
                 "the plan's tables need " + std::to_string(tile_off + tile_bytes) +
                     " bytes, more than the " + std::to_string(OPTCC_NOALLOC_SCRATCH_BYTES) +
@@ -167,6 +187,35 @@ int one_workgroup_per_cu_lds() {
     if (want > 0 && fixed + want <= per_block) v = want;
   }
   cache[dev] = v;
+  return v;
+}
+
+// Workgroups of the launch's kernel variant the whole device holds at once
+// (CUs x workgroups per CU at its registers and dynamic LDS), cached per
+// device and variant; 0 if the runtime cannot tell.
+int resident_workgroups(const KArgs &a, optcc_dtype_t dtype, bool servers, bool vec16, bool two) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int, int, int, int, int>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  const auto key = std::make_tuple(dev, (int)dtype, (int)servers, (int)vec16, (int)two,
+                                   servers ? a.g : 0, a.occ_lds);
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int per_cu = 0, cus = 0;
+  hipError_t err = hipSuccess;
+  switch (dtype) {
+    case OPTCC_F32: err = launch_f32(a, servers, vec16, two, nullptr, &per_cu); break;
+    case OPTCC_BF16: err = launch_bf16(a, servers, vec16, two, nullptr, &per_cu); break;
+    case OPTCC_F16: err = launch_f16(a, servers, vec16, two, nullptr, &per_cu); break;
+    default: err = launch_i32(a, servers, vec16, two, nullptr, &per_cu); break;
+  }
+  if (err != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    per_cu = cus = 0;
+  const int v = per_cu > 0 && cus > 0 ? per_cu * cus : 0;
+  cache[key] = v;
   return v;
 }
 
@@ -228,20 +277,56 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // slower at 2^22 (p = 8 and 128).
   const int vec_tile = kern::kThreads * (int)(16 / es);
   while (tile_elems > vec_tile && N / tile_elems < kTileMinCount) tile_elems /= 2;
-  DeviceTables dt;
-  int rc = noalloc ? scratch_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt)
-                   : device_tables(*pl, tile_elems, static_cast<hipStream_t>(stream), &dt);
-  if (rc != OPTCC_OK) return rc;
+
+  // Launch shape.  Short chains (inputs per lane: P' for one GPU per
+  // server, p for several): two vectors per lane (measured faster up to 32
+  // and neutral or slower beyond).  Longer chains run one workgroup per CU.
+  // Per-XCD tile runs: for short chains, for every server plan (beyond 32
+  // ranks, together with one workgroup per CU, 2.4-27 % faster than with
+  // neither) and for longer one-GPU-per-server chains whose tiles are more
+  // than one round of resident workgroups and at most kXcdRunsMaxTiles (p = 64
+  // and 128 at 2^19-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
+  // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower; with
+  // one round of tiles, 2^17-2^18 elements per rank, 3-5 % slower).
+  // bf16 with one GPU per server keeps full occupancy: eight elements per
+  // 16-byte vector, each widened by a shift, added in fp32 and rounded back,
+  // gain from the latency hiding of several waves (one workgroup per CU:
+  // p = 64 +0.5 %, p = 128 +1.5 %); bf16 server plans of more than 32 ranks
+  // gain from it (16 x 4 -3 %, 8 x 8 -1.3 %), like fp16, int32 and fp32.
+  // A single-hop chain (two healthy ranks, p = 3 with one straggler) runs
+  // one vector per lane in the identity order: 8 % faster than two vectors
+  // with XCD runs (p = 4 is fastest with both).
+  // Mid-size messages on short chains of 32-bit elements (3 to 7 healthy
+  // ranks, rank buffers of 16 MiB to 2 GiB in total) run one vector per lane
+  // in the identity order, in 1024-element tiles from 5 healthy ranks up.
+  // Measured (back-to-back calls, against two vectors with XCD runs): p = 8
+  // one straggler at 2^20-2^25 elements per rank 3-14 % faster (2^21:
+  // 29.9 -> 27.1 us, 2^22: 52.8 -> 48.0 us), int32 likewise; p = 6 at 2^22
+  // and 2^24 4-9 %; p = 4 (4096-element tiles) at 2^22 and 2^24 8-21 %; at
+  // 2 GiB (p = 8, 2^26) two vectors stay 4 % faster.
+  const bool servers = pl->kind == OPTCC_KIND_SERVERS;
+  const int chain = servers ? pl->p : pl->pp;
+  const bool long_chain = chain > kTwoVectorMaxHealthy;
+  const bool single_hop = !servers && pl->pp == 2;
+  const int64_t buf_bytes = (int64_t)p * N * (int64_t)es;
+  const bool mid_short = !servers && es == 4 && pl->pp >= 3 && pl->pp <= kOneVectorMaxHealthy &&
+                         buf_bytes >= kOneVectorMinBytes && buf_bytes < kOneVectorMaxBytes;
+  if (mid_short && pl->pp >= 5) tile_elems = std::min(tile_elems, vec_tile);
+  const int64_t ntiles = tile_count(*pl, tile_elems);
+  if (noalloc && scratch_bytes(*pl, ntiles) > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
+    return fail(OPTCC_EUNSUPPORTED,
+                "the plan's tables need " + std::to_string(scratch_bytes(*pl, ntiles)) +
+                    " bytes, more than the " + std::to_string(OPTCC_NOALLOC_SCRATCH_BYTES) +
+                    " of the no-allocation scratch array: use optcc_allreduce_emulate");
+  const bool two = !long_chain && !single_hop && !mid_short;
+  const bool two_vec = two && es == 4;  // two vectors per lane: 32-bit types only
+  hipStream_t st = static_cast<hipStream_t>(stream);
   KArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.tiles = dt.tiles;
-  a.segs = dt.segs;
-  a.ntiles = dt.ntiles;
   a.n = N;
   a.pp = pl->pp;
   a.m = pl->m;
   a.g = pl->g;
-  const bool servers = pl->kind == OPTCC_KIND_SERVERS;
   if (servers) {  // per server (healthy in ring order, then the straggler): its g GPUs
     const int g = pl->g;
     for (int h = 0; h < pl->pp; ++h)
@@ -251,39 +336,30 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
     for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   }
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  // short chains (inputs per lane: P' for one GPU per server, p for several):
-  // two vectors per lane (measured faster up to 32 and neutral or slower
-  // beyond).  Longer chains run one workgroup per CU.  Per-XCD tile runs:
-  // for short chains, for every server plan (beyond 32 ranks, together with
-  // one workgroup per CU, 2.4-27 % faster than with neither) and for longer
-  // one-GPU-per-server chains of at most kXcdRunsMaxTiles tiles (p = 64 and
-  // 128 at 2^20-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
-  // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower).
-  // bf16 with one GPU per server keeps full occupancy: eight elements per
-  // 16-byte vector, each widened by a shift, added in fp32 and rounded back,
-  // gain from the latency hiding of several waves (one workgroup per CU:
-  // p = 64 +0.5 %, p = 128 +1.5 %); bf16 server plans of more than 32 ranks
-  // gain from it (16 x 4 -3 %, 8 x 8 -1.3 %), like fp16, int32 and fp32.
-  // A single-hop chain (two healthy ranks, p = 3 with one straggler) runs
-  // one vector per lane in the identity order: 8 % faster than two vectors
-  // with XCD runs (p = 4 is fastest with both).
-  const int chain = servers ? pl->p : pl->pp;
-  const bool long_chain = chain > kTwoVectorMaxHealthy;
-  const bool single_hop = !servers && pl->pp == 2;
-  const bool two = !long_chain && !single_hop;
-  a.xcd_runs = servers || two || (long_chain && dt.ntiles <= kXcdRunsMaxTiles) ? 1 : 0;
   a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? one_workgroup_per_cu_lds() : 0;
+  bool runs = servers || two;
+  if (long_chain && !servers && ntiles <= kXcdRunsMaxTiles) {
+    const int resident = resident_workgroups(a, dtype, servers, vec16, two_vec);
+    runs = resident <= 0 || ntiles > resident;
+  }
+  a.xcd_runs = runs ? 1 : 0;
+  DeviceTables dt;
+  int rc = noalloc ? scratch_tables(*pl, tile_elems, st, &dt)
+                   : device_tables(*pl, tile_elems, st, &dt);
+  if (rc != OPTCC_OK) return rc;
+  a.tiles = dt.tiles;
+  a.segs = dt.segs;
+  a.ntiles = dt.ntiles;
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
     a.se = launches == 1 ? se : sb + l + 1;
     hipError_t err = hipSuccess;
     switch (dtype) {
-      case OPTCC_F32: err = launch_f32(a, servers, vec16, two, st); break;
-      case OPTCC_BF16: err = launch_bf16(a, servers, vec16, false, st); break;
-      case OPTCC_F16: err = launch_f16(a, servers, vec16, false, st); break;
-      default: err = launch_i32(a, servers, vec16, two, st); break;
+      case OPTCC_F32: err = launch_f32(a, servers, vec16, two_vec, st); break;
+      case OPTCC_BF16: err = launch_bf16(a, servers, vec16, two_vec, st); break;
+      case OPTCC_F16: err = launch_f16(a, servers, vec16, two_vec, st); break;
+      default: err = launch_i32(a, servers, vec16, two_vec, st); break;
     }
     if (err != hipSuccess)
       return fail(OPTCC_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(err));

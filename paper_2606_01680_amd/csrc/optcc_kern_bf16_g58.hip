@@ -4,8 +4,8 @@
 
 namespace optcc {
 
-hipError_t launch_bf16_g58(const kern::KArgs &a, bool two, hipStream_t st) {
-  return kern::launch_fixed_g<kern::BF16, 5, 6, 7, 8>(a, two, st);
+hipError_t launch_bf16_g58(const kern::KArgs &a, bool two, hipStream_t st, int *occ) {
+  return kern::launch_fixed_g<kern::BF16, 5, 6, 7, 8>(a, two, st, occ);
 }
 
 }  // namespace optcc

@@ -5,11 +5,12 @@
 
 namespace optcc {
 
-hipError_t launch_f16(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st) {
-  if (!servers) return kern::launch<kern::F16, false, 0>(a, vec16, two, st);
-  if (vec16 && a.g >= 2 && a.g <= 4) return kern::launch_fixed_g<kern::F16, 2, 3, 4>(a, two, st);
-  if (vec16 && a.g >= 5 && a.g <= 8) return launch_f16_g58(a, two, st);
-  return kern::launch<kern::F16, true, 0>(a, vec16, two, st);
+hipError_t launch_f16(const kern::KArgs &a, bool servers, bool vec16, bool two, hipStream_t st,
+                     int *occ) {
+  if (!servers) return kern::launch<kern::F16, false, 0>(a, vec16, two, st, occ);
+  if (vec16 && a.g >= 2 && a.g <= 4) return kern::launch_fixed_g<kern::F16, 2, 3, 4>(a, two, st, occ);
+  if (vec16 && a.g >= 5 && a.g <= 8) return launch_f16_g58(a, two, st, occ);
+  return kern::launch<kern::F16, true, 0>(a, vec16, two, st, occ);
 }
 
 }  // namespace optcc

@@ -61,6 +61,13 @@ constexpr int kTwoVectorMaxHealthy = 32;
 // longer one-GPU-per-server chains take per-XCD tile runs up to this many
 // tiles (measured faster at 2048 tiles and below, slower from 8192)
 constexpr int64_t kXcdRunsMaxTiles = 2048;
+// mid-size messages on one-GPU-per-server chains of 32-bit elements with at
+// most this many healthy ranks, whose rank buffers total at least
+// kOneVectorMinBytes and less than kOneVectorMaxBytes, run one vector per
+// lane in the identity tile order (measured faster than two vectors)
+constexpr int kOneVectorMaxHealthy = 7;
+constexpr int64_t kOneVectorMinBytes = (int64_t)16 << 20;
+constexpr int64_t kOneVectorMaxBytes = (int64_t)2 << 30;
 
 struct KArgs {
   const TileDesc *tiles;

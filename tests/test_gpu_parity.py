@@ -96,6 +96,33 @@ def test_tile_lengths_bit_exact(o, dtype, p, slow, n, k):
     assert bits_equal(got, ref)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+@pytest.mark.parametrize("p,slow,n,k", [
+    (8, {7: 0.875}, (1 << 20) + 12345, 64),   # 5 to 7 healthy: 1024-element tiles
+    (6, {0: 0.5}, (1 << 21) + 77, 16),
+    (7, {}, (1 << 20) + 3, 8),                  # no straggler: the ring
+    (4, {3: 0.5}, (1 << 22) + 999, 8),          # 3 healthy: the plan's own tile length
+    (9, {0: 0.875, 3: 0.75, 8: 0.5}, (1 << 20) + 64 * 5 + 1, 12),
+])
+def test_mid_size_short_chains_bit_exact(o, dtype, p, slow, n, k):
+    """Short chains of 32-bit elements whose rank buffers total 16 MiB to
+    2 GiB run one vector per lane in the identity tile order: every element
+    of every rank bit for bit against the oracle, ragged tails included."""
+    _say(f"case mid-size short chain dtype={dtype} p={p} slow={slow} n={n} k={k}")
+    x, ref, got = _run_both(o, p, slow, n, k, dtype, seed=61 + p)
+    assert bits_equal(got, ref)
+
+
+@pytest.mark.parametrize("p,n", [(40, 1 << 17), (64, 1 << 18), (64, (1 << 19) + 4097)])
+def test_long_chains_one_round_of_tiles(o, p, n):
+    """Long chains whose tiles fit in one round of resident workgroups take
+    the identity tile order, more tiles the per-XCD runs: both bit for bit."""
+    slow = {p - 1: 0.5, p - 2: 0.75}
+    _say(f"case long chain p={p} n={n}")
+    x, ref, got = _run_both(o, p, slow, n, 16, "f32", seed=7 + p)
+    assert bits_equal(got, ref)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 @pytest.mark.parametrize("p,slow", [(5, {0: 0.5}), (8, {7: 0.875}), (9, {0: 0.875, 3: 0.75, 8: 0.5}),
                                     (7, {}), (6, {1: 0.25, 2: 0.5})])
