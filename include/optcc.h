@@ -360,24 +360,29 @@ int optcc_plan_traffic(const optcc_plan_t *plan, optcc_dtype_t dtype, int slot_b
 /*
  * optcc_plan_timeline - evaluate the plan's schedule in the paper's network
  * model: start and finish time of every flow (in optcc_plan_get_flows order)
- * and the makespan, in the unit of optcc_model_time.
- *   - every rank has one send and one receive port, each carrying one flow at
- *     a time (Sec. 4.1: a NIC receives at most one flow at a time; Sec. 4.2:
- *     no NIC sends or receives two flows at once; full duplex);
- *   - a flow of len elements between ranks a and b lasts len * max(l_a, l_b)
- *     (Sec. 3 model with the time weighting of App. B.1);
- *   - a flow starts after the earlier steps of its section that wrote its
- *     source's or its destination's range have finished (Sec. 3: a rank sends
- *     only data it holds);
- *   - work-conserving list scheduling in priority order: flow order, except
- *     that with several stragglers the segments are taken in groups of four
- *     (one per pattern B, D, A', C'; the k/4 groups of App. D's time
- *     analysis), group by group, each group in flow order;
- *   - server plans (App. E bandwidth model): a flow between two GPUs of one
- *     server runs over NVLink, on that GPU pair's own NVLink send/receive
- *     ports, at (g-1) times NIC speed: it lasts len/(g-1).
- * The paper's own slot-level overlay of patterns A-D is given only as
- * figures; this is an evaluation of the same flows under the same rules.
+ * and the makespan, in the unit of optcc_model_time.  Model (Sec. 3, Sec. 4.1,
+ * App. B.1): every rank has one send and one receive port, each carrying one
+ * flow at a time (full duplex); a flow of len elements between ranks a and b
+ * lasts len * max(l_a, l_b); a flow starts after the earlier steps of its
+ * section that wrote its source's or its destination's range.
+ *   - one GPU per server: the paper's pattern overlay (Sec. 4.2, App. C,
+ *     App. D) as an explicit timetable of parallel bodies of P' + m - 1
+ *     windows: straggler s_i (worst first) receives from R[w-i+1] and sends to
+ *     R[w-i+2] in window w, every ring edge carries hop h of its chains in the
+ *     h-th window it is free, and each stage of a segment sits in the body
+ *     its pattern gives (one straggler: A and B from body 4q, C and D one body
+ *     later, k + 1 bodies; several: B, D, A', C' in k + 4 bodies; bubble
+ *     filling in the straggler windows).  With equal sections the windowed
+ *     timetable takes exactly the closed forms of Sec. 4.3 and App. C, and
+ *     App. D's body count.  The times returned run that timetable without
+ *     window boundaries: each port takes its flows in the timetable's order,
+ *     each as soon as both ports and its data are ready (never later).
+ *     Without straggler: the ring, one hop per window, T0 exactly.
+ *   - several GPUs per server (App. E, whose eight-row overlay is given only
+ *     as figures): work-conserving list scheduling in flow order and in
+ *     groups of eight segments per part, the shorter kept; a flow between
+ *     two GPUs of one server runs on their NVLink ports at (g-1) times NIC
+ *     speed (len/(g-1)).
  * start/finish may be NULL when cap = 0.  Errors: OPTCC_EINVAL,
  * OPTCC_EUNSUPPORTED (more than 2^26 flows), OPTCC_ENOMEM.
  */

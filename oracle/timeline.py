@@ -32,6 +32,9 @@ Rules (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
 Times are exact rationals (``fractions.Fraction``), so there are no ties to
 break by tolerance (the library, in doubles, merges events closer than 1e-9 of
 the current time).  The naive scan is quadratic: small schedules only.
+
+``construction`` times the same flows by the paper's own pattern overlay
+instead (an explicit timetable, no scheduling policy): see its notes below.
 """
 from __future__ import annotations
 
@@ -176,3 +179,163 @@ def validate(sched, bandwidths, times):
             if F(s) < step_end[d] - F(1, 10**6) * max(1, step_end[d]):
                 errs.append(f"step {i} starts before its dependency {d} ends")
     return errs
+
+
+# ------------------------------------------------ the paper's construction
+# The pattern overlay of Sec. 4.2 (one straggler) and App. D (several),
+# rebuilt from the text as an explicit timetable of parallel bodies and
+# windows (the flow-grid figures are missing; every choice the text leaves
+# open is a reading listed with the design notes):
+#
+# * A body has W = P' + m - 1 windows (P' healthy ranks R[0..P'-1] in ring
+#   order, m stragglers s_1..s_m worst first; App. D: p - 1 windows, p - m - 1
+#   of them carrying ring flows and m straggler traffic, per rank).
+#   Straggler s_i serves windows i-1 .. i-1+P'-1: in window w it receives
+#   from R[w-i+1] (Stage 2, or the point-to-point upload of bubble filling)
+#   and sends to the next rank R[w-i+2] (Stage 3, or the download).  So in
+#   window w the ring edges R[e] -> R[e+1] with w-m+1 <= e <= w are idle.
+# * Ring stages (Stage 1 and Stage 4 of two segments per body, two
+#   sub-slots per window): the h-th window in which edge e is not idle
+#   carries hop h of the chain that crosses edge e at its h-th hop.  Every
+#   chain then crosses its edges in order, and every non-idle edge carries
+#   one flow per sub-slot.
+# * Pattern overlay (Sec. 4.2, App. D): segment g is pattern g mod 4 of
+#   group g div 4; a pattern puts each stage of its segment in one body.
+#   One straggler: A = S1 S2 S3 S4 from body 4q, B = S3 S1 S4 S2 from body
+#   4q, C and D the same one body later; so a group spans five bodies and
+#   overlaps the next by one: k + 1 bodies (Sec. 4.3).  Several stragglers
+#   (B, D, A', C'): B from body 4q, D from 4q + 2, A' (S1 in body 4q + 1)
+#   and C' (S1 in 4q + 3) with their non-finalising stragglers' raw values
+#   two bodies before Stage 1 and the global sum delivered to them in the
+#   Stage 4 body: a group spans eight bodies, k + 4 in all (App. D).
+# * Bubble filling (App. C): the point-to-point chunk of segment g goes up
+#   in body g (after the Stage 2 flow of the same window, from the same
+#   rank) and down in body g + 1 (after the Stage 3 flow).
+# * Timing: window after window; a window lasts as long as its longest lane
+#   (a ring edge's two sub-slots, or a straggler's receive or send flows
+#   back to back).
+# Without straggler the ring runs its segments one after another, Stage 1
+# then Stage 4, one hop per window.
+
+# body offsets of each stage within a group (keys: slot of the step;
+# "raw"/"sum" for the non-finalising stragglers of A'/C')
+_OVERLAY_ONE = [  # A, B, C, D
+    {1: 0, 2: 1, 3: 2, 4: 3},
+    {0: 0, 1: 1, 4: 2, 5: 3},
+    {1: 1, 2: 2, 3: 3, 4: 4},
+    {0: 1, 1: 2, 4: 3, 5: 4},
+]
+_OVERLAY_MULTI = [  # B, D, A', C'
+    {0: 0, 1: 1, 4: 2, 5: 3},
+    {0: 2, 1: 3, 4: 4, 5: 5},
+    {0: -1, 1: 1, 2: 2, 3: 3, 4: 4, 5: 4},
+    {0: 1, 1: 3, 2: 4, 3: 5, 4: 6, 5: 6},
+]
+
+
+def construction(sched, bandwidths, asap=False):
+    """(makespan, [(start, finish) per flow in flow order], info) of the
+    paper's pattern-overlay timetable for a one-GPU-per-server schedule.
+    info: number of bodies, and the duration of every body (window by
+    window).  asap=True runs the same timetable without its window
+    boundaries: every port takes its flows in the timetable's order, each as
+    soon as the port, the other port and the flow's data are ready (never
+    later than the windowed timetable)."""
+    if getattr(sched, "g", 1) > 1:
+        raise ValueError("the construction covers one GPU per server")
+    steps = sched.steps()
+    ell = rank_slowdowns(sched, bandwidths)
+    pp, m = sched.pp, sched.m
+    pos = {int(r): i for i, r in enumerate(sched.ring)}
+    strag = {int(r): i + 1 for i, r in enumerate(sched.stragglers)}  # s_i, 1-based
+    W = pp + m - 1 if m else pp - 1
+    overlay = _OVERLAY_ONE if m == 1 else _OVERLAY_MULTI
+
+    def active_window(e, h):
+        """Window of hop h on edge e (the h-th window in which e is not idle)."""
+        return h if h < e else h + m
+
+    lanes = {}  # (body, window) -> lane -> [(order, flow id)]
+    flows = []
+    seen = {}  # steps so far of each (slot, segment, section): the hop
+    for i, st in enumerate(steps):
+        key = (st["slot"], st["seg"], st["sec"])
+        h = seen.get(key, 0)
+        seen[key] = h + 1
+        for src in st["srcs"]:
+            dst = st["dst"]
+            dur = st["len"] * max(ell[src], ell[dst])
+            f = len(flows)
+            flows.append(dur)
+            g, slot, sec = st["seg"], st["slot"], st["sec"]
+            q, pat = divmod(g, 4)
+            if m == 0:  # the ring: segment after segment, S1 then S4
+                body = 2 * g + (0 if slot == 1 else 1)
+                e = pos[src]
+                cell, lane, sub = (body, h), ("edge", e), 0
+            elif sec < 0:  # bubble filling: up in body g, down in body g + 1
+                if slot == 2:
+                    a = pos[src]
+                    cell, lane, sub = (g, a), ("recv", 1), 1
+                else:
+                    b = pos[dst]
+                    cell, lane, sub = (g + 1, (b - 1) % pp), ("send", 1), 1
+            elif slot in (1, 4):  # ring stages
+                e = pos[src]
+                body = 4 * q + overlay[pat][slot]
+                cell, lane, sub = (body, active_window(e, h)), ("edge", e), g
+            else:  # a straggler flow
+                off = overlay[pat][slot]
+                body = 4 * q + off
+                if dst in strag:  # received by s_i from R[a]
+                    i_s, a = strag[dst], pos[src]
+                    cell, lane = (body, a + i_s - 1), ("recv", i_s)
+                else:  # sent by s_i to R[b]
+                    i_s, b = strag[src], pos[dst]
+                    cell, lane = (body, (b - 1) % pp + i_s - 1), ("send", i_s)
+                sub = 0
+            lanes.setdefault(cell, {}).setdefault(lane, []).append((sub, f))
+    start = [None] * len(flows)
+    finish = [None] * len(flows)
+    if asap:
+        return _asap(sched, steps, ell, lanes, flows) + ({},)
+    t = F(0)
+    body_len = {}
+    for cell in sorted(lanes):
+        t0 = t
+        end = t0
+        for lane, fl in lanes[cell].items():
+            x = t0
+            for _, f in sorted(fl):
+                start[f], finish[f] = x, x + flows[f]
+                x = finish[f]
+            end = max(end, x)
+        body_len[cell[0]] = body_len.get(cell[0], F(0)) + (end - t0)
+        t = end
+    info = {"bodies": len(body_len), "body_durations": [body_len[b] for b in sorted(body_len)],
+            "windows_per_body": W}
+    return t, list(zip(start, finish)), info
+
+
+def _asap(sched, steps, ell, lanes, durations):
+    """The windowed timetable's flows, taken in its order (window, lane,
+    position), each started as soon as its send port, its receive port and
+    the steps it depends on are done."""
+    deps = dependencies(steps)
+    step_of = []
+    for i, st in enumerate(steps):
+        for src in st["srcs"]:
+            step_of.append((i, src, st["dst"]))
+    send_free, recv_free, step_end = {}, {}, {}
+    start = [None] * len(durations)
+    finish = [None] * len(durations)
+    for cell in sorted(lanes):
+        for lane, fl in sorted(lanes[cell].items(), key=lambda kv: str(kv[0])):
+            for _, f in sorted(fl):
+                i, a, b = step_of[f]
+                t = max([send_free.get(a, F(0)), recv_free.get(b, F(0))] +
+                        [step_end[d] for d in deps[i]])
+                start[f], finish[f] = t, t + durations[f]
+                send_free[a] = recv_free[b] = finish[f]
+                step_end[i] = max(step_end.get(i, F(0)), finish[f])
+    return max(finish, default=F(0)), list(zip(start, finish))

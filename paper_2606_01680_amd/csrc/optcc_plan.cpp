@@ -4,6 +4,7 @@
 //
 // Paper: "Don't Let a Few Network Failures Slow the Entire AllReduce".
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <exception>
@@ -692,7 +693,10 @@ extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, i
 
 // ------------------------------------------------------------- timeline
 // Evaluation of the plan's flows in the paper's network model (Sec. 3 model;
-// Sec. 4.1 flow rule; App. B.1 time weighting):
+// Sec. 4.1 flow rule; App. B.1 time weighting).  Plans with one GPU per
+// server are timed by the paper's own pattern overlay (overlay_timeline,
+// below); plans with several GPUs per server, whose eight-row overlay App. E
+// gives only as figures, by list scheduling (list_timeline):
 //  * every rank has a send port and a receive port (full duplex), each
 //    carrying at most one flow at a time;
 //  * a flow of len elements between ranks a and b lasts len * max(l_a, l_b);
@@ -714,12 +718,11 @@ extern "C" int optcc_plan_traffic(const optcc_plan_t *pl, optcc_dtype_t dtype, i
 // one server runs over NVLink, on separate NVLink send/receive ports, at
 // (g-1) times NIC speed (len/(g-1)); flows between servers use the NICs.
 // Times are doubles; events closer than 1e-9 of the current time are merged.
-extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double *finish,
-                                   int64_t cap, double *makespan) {
-  if (!pl || !makespan) return fail(OPTCC_EINVAL, "plan and makespan must be non-NULL");
-  if (cap > 0 && (!start || !finish)) return fail(OPTCC_EINVAL, "start/finish are NULL");
-  if (pl->num_flows > ((int64_t)1 << 26))
-    return fail(OPTCC_EUNSUPPORTED, "timeline limited to 2^26 flows");
+namespace optcc {
+namespace {
+
+int list_timeline(const optcc_plan_t *pl, double *start, double *finish, int64_t cap,
+                  double *makespan) {
   try {
     // steps and flows in execution order
     std::vector<int32_t> st_dst, f_src, f_dst;  // flows: send and receive port ids
@@ -888,4 +891,193 @@ extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double
     return fail(OPTCC_ENOMEM, std::string("timeline: ") + e.what());
   }
   return OPTCC_OK;
+}
+
+// The paper's pattern overlay (Sec. 4.2 for one straggler, App. D for
+// several, Sec. 4.3 and App. C for the timing) as an explicit timetable;
+// the flow grids of the paper are figures, so the layout below is rebuilt
+// from the text:
+//  * a parallel body has W = P' + m - 1 windows (App. D: p - 1 windows per
+//    body, p - m - 1 of them with ring flows and m with straggler traffic,
+//    per rank).  Straggler s_i (i = 1 the worst) takes windows i-1 ..
+//    i-1+P'-1: in window w it receives from healthy rank R[w-i+1] and sends
+//    to the next one, R[w-i+2], so the ring edges R[e] -> R[e+1] with
+//    w-m+1 <= e <= w carry nothing in window w;
+//  * ring stages: each body holds Stage 1 or Stage 4 of two segments, one per
+//    sub-slot, earlier segment first; the h-th window in which an edge
+//    carries ring flows carries hop h of the chain that crosses it at hop h;
+//  * stage bodies per pattern (segment g = pattern g mod 4 of group g div 4,
+//    offsets from body 4 (g div 4)): one straggler A = S1 S2 S3 S4 at
+//    0..3, B = S3 S1 S4 S2 at 0..3, C and D the same one body later (k + 1
+//    bodies, Sec. 4.3); several stragglers B = S3 S1 S4 S2 at 0..3, D at
+//    2..5, A' with S1 at 1, C' with S1 at 3 (S2, S3, S4 in the next bodies),
+//    the non-finalising stragglers' raw values two bodies before Stage 1 and
+//    the global sum to them in the Stage 4 body (k + 4 bodies, App. D);
+//  * bubble filling (App. C): segment g's point-to-point chunk goes up in
+//    body g after the Stage 2 flow of the same sender and window, and down
+//    in body g + 1 after the Stage 3 flow;
+//  * windows run one after another; a window lasts as long as its longest
+//    lane (an edge's two sub-slots, or a straggler's receive or send flows
+//    back to back).
+// Without straggler the ring takes its segments one after another, Stage 1
+// then Stage 4, one hop per window (T0 exactly).  The timeline returned runs
+// that timetable without its window boundaries: every port takes its flows
+// in the timetable's order (window, lane, position), each as soon as both its
+// ports are free and the steps it depends on are done, which is never later
+// than the windowed timetable (with equal sections the two agree on the
+// closed forms of Sec. 4.3 and App. C; the section sizes' rounding to whole
+// quanta makes windows wait for their longest lane).
+int overlay_timeline(const optcc_plan_t &pl, double *start, double *finish, int64_t cap,
+                     double *makespan) {
+  constexpr int X = INT32_MIN;  // the pattern has no such slot
+  static const int kOne[4][OPTCC_NUM_SLOTS] = {
+      {X, 0, 1, 2, 3, X}, {0, 1, X, X, 2, 3}, {X, 1, 2, 3, 4, X}, {1, 2, X, X, 3, 4}};
+  static const int kMulti[4][OPTCC_NUM_SLOTS] = {
+      {0, 1, X, X, 2, 3}, {2, 3, X, X, 4, 5}, {-1, 1, 2, 3, 4, 4}, {1, 3, 4, 5, 6, 6}};
+  try {
+    const int pp = pl.pp, m = pl.m;
+    const int64_t W = m > 0 ? pp + m - 1 : pp - 1;
+    std::vector<int> ring_pos((size_t)pl.p, -1), strag_no((size_t)pl.p, 0);
+    for (int i = 0; i < pp; ++i) ring_pos[(size_t)pl.ring[(size_t)i]] = i;
+    for (int i = 0; i < m; ++i) strag_no[(size_t)pl.strag[(size_t)i]] = i + 1;
+    const auto &tab = m == 1 ? kOne : kMulti;
+    struct Place {
+      int64_t cell;   // body * W + window (bodies shifted to start at 0)
+      int32_t lane;   // ring edge e, or pp + 2(i-1) (+1 for sends) for straggler i
+      int32_t order;  // within the lane: the segment (ring) or 0/1 (straggler)
+      int64_t flow;
+      double dur;
+    };
+    std::vector<Place> pl_of;
+    pl_of.reserve((size_t)pl.num_flows);
+    // per flow: sender, receiver, step; per step: the steps it depends on
+    // (earlier steps of its section that last wrote its sources or its
+    // destination)
+    std::vector<int32_t> f_src, f_dst;
+    std::vector<int64_t> f_step, dep_first(1, 0), dep_list;
+    f_src.reserve((size_t)pl.num_flows);
+    f_dst.reserve((size_t)pl.num_flows);
+    f_step.reserve((size_t)pl.num_flows);
+    std::unordered_map<uint64_t, int64_t> last_writer;  // (rank, seg, sec) -> step
+    auto wkey = [](int rank, int seg, int sec) {
+      return ((uint64_t)(uint32_t)rank << 40) | ((uint64_t)(uint32_t)seg << 12) | (uint64_t)(sec + 1);
+    };
+    int64_t nf = 0, nsteps = 0;
+    int last_slot = -1, last_seg = -1, last_sec = -2, hop = 0;
+    const int64_t shift = m >= 2 ? 1 : 0;  // the head body of A' is body -1
+    for_each_step(pl, [&](int slot, int g, int sec, int, int dst, const int *srcs, int ns,
+                          int64_t, int64_t len) {
+      if (slot == last_slot && g == last_seg && sec == last_sec) {
+        ++hop;
+      } else {
+        hop = 0;
+        last_slot = slot;
+        last_seg = g;
+        last_sec = sec;
+      }
+      const int64_t sid = nsteps++;
+      const size_t d0 = dep_list.size();
+      auto dep = [&](int rank) {
+        auto it = last_writer.find(wkey(rank, g, sec));
+        if (it != last_writer.end() &&
+            std::find(dep_list.begin() + (ptrdiff_t)d0, dep_list.end(), it->second) == dep_list.end())
+          dep_list.push_back(it->second);
+      };
+      for (int i = 0; i < ns; ++i) dep(srcs[i]);
+      dep(dst);
+      dep_first.push_back((int64_t)dep_list.size());
+      last_writer[wkey(dst, g, sec)] = sid;
+      for (int i = 0; i < ns; ++i, ++nf) {
+        const int src = srcs[i];
+        f_src.push_back(src);
+        f_dst.push_back(dst);
+        f_step.push_back(sid);
+        Place q;
+        q.flow = nf;
+        q.dur = (double)len * std::max(pl.ell[(size_t)src], pl.ell[(size_t)dst]);
+        int64_t body, window;
+        if (m == 0) {  // the ring: segment by segment, Stage 1 then Stage 4
+          body = 2 * (int64_t)g + (slot == 1 ? 0 : 1);
+          window = hop;
+          q.lane = ring_pos[(size_t)src];
+          q.order = 0;
+        } else if (sec < 0) {  // bubble filling
+          if (slot == 2) {
+            body = g;
+            window = ring_pos[(size_t)src];
+            q.lane = pp;
+          } else {
+            body = (int64_t)g + 1;
+            window = (ring_pos[(size_t)dst] + pp - 1) % pp;
+            q.lane = pp + 1;
+          }
+          q.order = 1;
+        } else if (slot == 1 || slot == 4) {  // ring stages
+          const int e = ring_pos[(size_t)src];
+          body = 4 * (int64_t)(g / 4) + tab[g % 4][slot];
+          window = hop < e ? hop : hop + m;
+          q.lane = e;
+          q.order = g;
+        } else {  // straggler traffic
+          body = 4 * (int64_t)(g / 4) + tab[g % 4][slot];
+          if (strag_no[(size_t)dst] > 0) {  // received by s_i from R[a]
+            const int si = strag_no[(size_t)dst], a = ring_pos[(size_t)src];
+            window = a + si - 1;
+            q.lane = pp + 2 * (si - 1);
+          } else {  // sent by s_i to R[b]
+            const int si = strag_no[(size_t)src], b = ring_pos[(size_t)dst];
+            window = (b + pp - 1) % pp + si - 1;
+            q.lane = pp + 2 * (si - 1) + 1;
+          }
+          q.order = 0;
+        }
+        q.cell = (body + shift) * W + window;
+        pl_of.push_back(q);
+      }
+    });
+    std::sort(pl_of.begin(), pl_of.end(), [](const Place &x, const Place &y) {
+      if (x.cell != y.cell) return x.cell < y.cell;
+      if (x.lane != y.lane) return x.lane < y.lane;
+      return x.order < y.order;
+    });
+    // The timetable's order is a valid execution order (every port's flows
+    // in sequence, every step after the steps it depends on): run it with
+    // each flow starting as soon as it can.
+    std::vector<double> fs((size_t)nf), ff((size_t)nf), send_free((size_t)pl.p, 0.0),
+        recv_free((size_t)pl.p, 0.0), step_end((size_t)nsteps, 0.0);
+    double t = 0.0;
+    for (const Place &q : pl_of) {
+      const int64_t f = q.flow, sid = f_step[(size_t)f];
+      const int a = f_src[(size_t)f], b = f_dst[(size_t)f];
+      double x = std::max(send_free[(size_t)a], recv_free[(size_t)b]);
+      for (int64_t d = dep_first[(size_t)sid]; d < dep_first[(size_t)sid + 1]; ++d)
+        x = std::max(x, step_end[(size_t)dep_list[(size_t)d]]);
+      fs[(size_t)f] = x;
+      ff[(size_t)f] = x + q.dur;
+      send_free[(size_t)a] = recv_free[(size_t)b] = ff[(size_t)f];
+      step_end[(size_t)sid] = std::max(step_end[(size_t)sid], ff[(size_t)f]);
+      t = std::max(t, ff[(size_t)f]);
+    }
+    for (int64_t f = 0; f < std::min(cap, nf); ++f) {
+      start[f] = fs[(size_t)f];
+      finish[f] = ff[(size_t)f];
+    }
+    *makespan = t;
+  } catch (const std::bad_alloc &) {
+    return fail(OPTCC_ENOMEM, "out of host memory");
+  }
+  return OPTCC_OK;
+}
+
+}  // namespace
+}  // namespace optcc
+
+extern "C" int optcc_plan_timeline(const optcc_plan_t *pl, double *start, double *finish,
+                                   int64_t cap, double *makespan) {
+  if (!pl || !makespan) return fail(OPTCC_EINVAL, "plan and makespan must be non-NULL");
+  if (cap > 0 && (!start || !finish)) return fail(OPTCC_EINVAL, "start/finish are NULL");
+  if (pl->num_flows > ((int64_t)1 << 26))
+    return fail(OPTCC_EUNSUPPORTED, "timeline limited to 2^26 flows");
+  if (pl->kind == OPTCC_KIND_SERVERS) return list_timeline(pl, start, finish, cap, makespan);
+  return overlay_timeline(*pl, start, finish, cap, makespan);
 }

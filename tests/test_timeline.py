@@ -1,8 +1,12 @@
 """Evaluated schedule (the plan's flows timed in the paper's network model).
 
-The library's timeline must equal the oracle's exact-rational evaluation of
-the same rules flow by flow, and pass the oracle's policy-free validator.
-The validator itself is checked by planting mistakes in a valid timeline.
+Plans with one GPU per server are timed by the paper's pattern overlay
+(`tests/test_timetable.py` pins it against the time analyses); here the
+library's timeline of the workloads and of ragged plans is compared with the
+oracle's exact run and the policy-free validator, and the validator itself is
+checked by planting mistakes in a valid timeline.  Plans with several GPUs per
+server are timed by list scheduling (App. E's overlay is given only as
+figures), compared the same way.
 """
 from fractions import Fraction as F
 
@@ -32,7 +36,6 @@ CASES = [
     (5, {0: 2 / 3}, 52 * 64 * 4, 4), (6, {2: 0.75}, 3000, 4), (8, {7: 0.875}, 64 * 7 * 8 * 4, 8),
     (7, {0: 0.5, 1: 0.75}, 64 * 5 * 8 * 4, 8), (9, {0: 0.875, 3: 0.75, 8: 0.5}, 4000, 4),
     (6, {5: 0.25}, 64 * 5 * 4, 4),
-    # several stragglers over three and four pattern groups (the group order wins)
     (6, {1: 0.5, 4: 0.875}, 64 * 4 * 12 * 2, 12), (9, {2: 0.75, 5: 0.5, 6: 0.5}, 64 * 6 * 16, 16),
 ]
 
@@ -41,7 +44,7 @@ CASES = [
 def test_timeline_equals_oracle(o, p, slow, n, k):
     bw = _bw(p, slow)
     sched = oracle.Schedule(p, bw, n, k)
-    mk_ref, ref = T.evaluate(sched, bw)
+    mk_ref, ref, _ = T.construction(sched, bw, asap=True)
     pl = o.optcc_plan(p, bw, n, k)
     mk, st, fi = pl.timeline()
     scale = max(1.0, float(mk_ref))
@@ -55,21 +58,12 @@ def test_timeline_equals_oracle(o, p, slow, n, k):
 @pytest.mark.parametrize("p,slow,n,k", CASES)
 def test_evaluated_respects_lower_bound(p, slow, n, k):
     """Theorems 1/2 and the tight bound hold for any correct AllReduce, so
-    also for this evaluated schedule."""
+    also for the timetable and its as-soon-as-possible run."""
     bw = _bw(p, slow)
-    mk, _ = T.evaluate(oracle.Schedule(p, bw, n, k), bw)
-    assert mk >= model.lower_bound(bw, n)
-
-
-@pytest.mark.parametrize("p", [3, 4, 7, 9])
-def test_ring_attains_t0(p):
-    """Sec. 3: without stragglers the ring reaches T0 = 2(p-1)n/p exactly when
-    every section has the same size."""
-    k = 4
-    n = p * 64 * k * 3
-    bw = [1.0] * p
-    mk, _ = T.evaluate(oracle.Schedule(p, bw, n, k), bw)
-    assert mk == model.t0(p, n)
+    sched = oracle.Schedule(p, bw, n, k)
+    for asap in (False, True):
+        mk, _, _ = T.construction(sched, bw, asap=asap)
+        assert mk >= model.lower_bound(bw, n)
 
 
 def test_validator_catches_planted_mistakes():
@@ -77,7 +71,7 @@ def test_validator_catches_planted_mistakes():
     and a flow that starts before the data it forwards exists."""
     p, bw, n, k = 5, [0.5, 1, 1, 1, 1], 64 * 4 * 4, 4
     sched = oracle.Schedule(p, bw, n, k)
-    _, good = T.evaluate(sched, bw)
+    _, good, _ = T.construction(sched, bw)
     assert T.validate(sched, bw, good) == []
     flows = [(st["slot"], src, st["dst"]) for st in sched.steps() for src in st["srcs"]]
     # shorten the first flow
@@ -98,10 +92,10 @@ def test_validator_catches_planted_mistakes():
 @pytest.mark.parametrize("w", ["p4_f32", "p8_f32", "p16_bf16", "p64_f32",
                                pytest.param("p128_f32", marks=pytest.mark.slow)])
 def test_workload_evaluated_times(o, w):
-    """Full-size evaluated makespans against the closed forms and bounds:
-    p4 and p16 (l = 2) at or below (k+1)/k l n, p8 (bubble filling) within
-    1 % of its closed form, p64 and p128 (two and four stragglers, taken in
-    pattern groups) at or below (k+4) T_body (App. D); always above the best
+    """Full-size timelines against the closed forms and bounds: one
+    straggler within 0.5 % of Sec. 4.3 / App. C (the sections' whole quanta
+    differ by one quantum: p4 +0.3 %, p8 and p16 below 0.01 %), several
+    stragglers at or below (k+4) T_body (App. D); always above the best
     lower bound."""
     from paper_2606_01680_amd.workloads import WORKLOADS
     W = WORKLOADS[w]
@@ -110,10 +104,10 @@ def test_workload_evaluated_times(o, w):
     closed = o.optcc_model_time(pl)
     lb = o.optcc_lower_bound(W.p, W.bandwidths, W.n)
     assert mk >= lb * (1 - 1e-12)
-    if pl.kind in ("single_ge2", "multi"):
+    if pl.kind == "multi":
         assert mk <= closed * (1 + 1e-12)
     else:
-        assert mk <= closed * 1.01
+        assert mk <= closed * 1.005
 
 
 # ------------------------------------------------ several GPUs per server
