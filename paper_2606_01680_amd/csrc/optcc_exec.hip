@@ -337,6 +337,13 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   }
   a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? one_workgroup_per_cu_lds() : 0;
+  // The same mid-size short chains take each vector's Stage 4 stores into
+  // the next vector's Stage 1 chain (the kernel's pipelined ring tiles).
+  // Measured against one vector at a time (back-to-back calls, every result
+  // bit for bit equal): p = 8 fp32 at 2^20 / 2^21 / 2^22 elements per rank
+  // 3 / 1.2 / 1.5 % faster, int32 at 2^22 1.7 %, 2^24 equal; long chains
+  // lose 1-8 % (p = 64, 128), so they keep one vector at a time.
+  a.pipe = mid_short ? 1 : 0;
   bool runs = servers || two;
   if (long_chain && !servers && ntiles <= kXcdRunsMaxTiles) {
     const int resident = resident_workgroups(a, dtype, servers, vec16, two_vec);

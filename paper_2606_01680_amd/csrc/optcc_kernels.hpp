@@ -82,6 +82,10 @@ struct KArgs {
   // workgroup.  Reserving more than half of a CU's LDS holds the launch to
   // one workgroup per CU.
   int32_t occ_lds;
+  // 1: the ring lanes of a whole AllReduce (slots [0, 6)) with one vector
+  // per lane defer each vector's Stage 4 stores into the next vector's
+  // Stage 1 chain (pipelined_ring_tile)
+  int32_t pipe;
   // rank pointers.  g = 1: [0, pp) healthy ranks in ring order, [pp, pp+m)
   // stragglers sorted by slowdown (worst first).  g > 1: [h*g, h*g+g) the g
   // GPUs (by local index) of the h-th healthy server in ring order, then the
@@ -754,6 +758,80 @@ __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
   return sd.nbig + (int)((u - big) / (uint32_t)sd.qbase);
 }
 
+// Every ring-section vector of one tile's lane, for a whole AllReduce
+// (slots [0, 6)), one GPU per server, one vector at a time: vector v's
+// Stage 1 chain carries, one per hop, the Stage 4 stores of vector v - 1,
+// and the stragglers' copies of vector v - 1 follow the chain, so that a
+// wave keeps loads in flight while it writes the previous vector's
+// allgather.  Each vector gets exactly the steps ring_lane gives it (other
+// coordinates only move in time), so the result is the same bit for bit.
+// Elements past the last whole vector of the tile are left to the caller.
+template <class D, int W, int B>
+__device__ void pipelined_ring_tile(const KArgs &a, void *const *rp, const SegDesc &sd,
+                                    int64_t e0, int64_t end, int64_t stride) {
+  using V = Vec<D, W>;
+  const int pp = a.pp, m = a.m;
+  const int ord = sd.ordering;
+  const int nside = m == 0 ? 0 : (ord == 2 ? m : m - 1);
+  const int sfirst = ord == 2 ? 0 : 1;
+  const bool fin = m >= 1 && ord == 1;
+  const int nh = pp - 1;
+  bool pend = false;  // vector v - 1 still owes its Stage 4 and slot-5 stores
+  V vp;
+  int jp = 0;
+  int64_t ep = 0;
+  auto rank_at = [&](int j, int t) {  // buffer of R[j + t], 0 <= t < 2 pp
+    int i = j + t;
+    return rp[i >= pp ? i - pp : i];
+  };
+  for (; e0 + W <= end; e0 += stride) {
+    const int j = section_of(sd, (e0 - sd.ring_begin) / kQuantum);
+    V xs;
+    if (fin) xs = ld_in<D, W>(a.ptr[pp], e0);
+    V v;
+    if (nside > 0) {  // slot 0: stragglers' raw values into the chain start
+      AccV<D, W> acc = widen(ld_in<D, W>(rp[j], e0));
+      for (int i = 0; i < nside; ++i) accum(acc, ld_in<D, W>(a.ptr[pp + sfirst + i], e0));
+      v = narrow(acc);
+      st_mid<D, W>(rp[j], e0, v);
+    } else {
+      v = ld_in<D, W>(rp[j], e0);
+    }
+    // slot 1: the chain, with a rolling window of B hop loads; hop t also
+    // stores the t-th Stage 4 value of the previous vector
+    V buf[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+      if (u < nh) buf[u] = ld_in<D, W>(rank_at(j, 1 + u), e0);
+    for (int t = 0; t < nh; t += B) {
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (t + u < nh) {
+          v = add2<D, W>(buf[u], v);
+          st_mid<D, W>(rank_at(j, 1 + t + u), e0, v);
+          if (t + u + B < nh) buf[u] = ld_in<D, W>(rank_at(j, 1 + t + u + B), e0);
+          if (pend) st_fin<D, W>(rank_at(jp, t + u), ep, vp);
+        }
+    }
+    if (pend) {  // slot 5 of the previous vector
+      for (int i = 0; i < nside; ++i) st_fin<D, W>(a.ptr[pp + sfirst + i], ep, vp);
+    }
+    if (fin) {  // slots 2 and 3: the finalising straggler and back to the holder
+      v = add2<D, W>(xs, v);
+      st_fin<D, W>(a.ptr[pp], e0, v);
+      st_fin<D, W>(rank_at(j, pp - 1), e0, v);
+    }
+    pend = true;
+    vp = v;
+    jp = j;
+    ep = e0;
+  }
+  if (pend) {
+    for (int t = 0; t + 1 < pp; ++t) st_fin<D, W>(rank_at(jp, t), ep, vp);
+    for (int i = 0; i < nside; ++i) st_fin<D, W>(a.ptr[pp + sfirst + i], ep, vp);
+  }
+}
+
 template <class D, int W, int L, int B, bool S, int G>
 __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const SegDesc &sd,
                                           bool p2p, const int64_t (&e)[L]) {
@@ -800,6 +878,20 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
     const SegDesc sd = a.segs[td.meta >> 1];
     const int64_t end = td.begin + td.len;
     int64_t e0 = td.begin + (int64_t)threadIdx.x * W;
+    if constexpr (!S && L == 1) {
+      if (a.pipe && !p2p && a.sb == 0 && a.se == OPTCC_NUM_SLOTS) {
+        pipelined_ring_tile<D, W, B>(a, rp, sd, e0, end, kStride);
+        // elements past the last whole vector (only at the end of the rank
+        // vectors) one by one
+        int64_t x = e0 + (end - W - e0 >= 0 ? ((end - W - e0) / kStride + 1) * kStride : 0);
+        for (; x < end; x += kStride)
+          for (int64_t y = x; y < end && y < x + W; ++y) {
+            const int64_t e[1] = {y};
+            run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
+          }
+        continue;
+      }
+    }
     for (; e0 + (L - 1) * kStride + W <= end; e0 += L * kStride) {
       int64_t e[L];
 #pragma unroll
