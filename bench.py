@@ -348,7 +348,12 @@ def measure(torch, optcc, w, args, check=True):
         "GBps": round(alg_bytes / (ms_step * 1e-3) / 1e9, 2),
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
+            "frac": round(achieved / PEAK_GBPS, 4),
+            "basis": "achieved and frac: algorithmic bytes (every rank input read once, "
+                     "every step's destination written) per mean launch time; traffic_GBps "
+                     "and traffic_frac: rocprofv3 FETCH_SIZE + WRITE_SIZE bytes (L2 to "
+                     "memory fabric) per launch",
+            "traffic": traffic,
             "traffic_GBps": None if traffic is None else round(traffic / (ms_launch * 1e-3) / 1e9, 2),
             "traffic_frac": None if traffic is None else round(
                 traffic / (ms_launch * 1e-3) / 1e9 / PEAK_GBPS, 4),
@@ -484,6 +489,7 @@ def main():
         "metric": METRIC,
         "value": rec["GBps"],
         "unit": "GB/s",
+        "value_basis": "algorithmic bytes of the AllReduce's steps / ms_per_step",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
