@@ -318,8 +318,8 @@ int optcc_plan_segments(const optcc_plan_t *plan, int64_t *offset, int64_t *leng
 #define OPTCC_STAGE_N3 7
 #define OPTCC_STAGE_N4 8
 
-/* One flow: a point-to-point transfer of one section (or one bubble-filling
- * chunk) from one rank to another (Sec. 4.1 defines a flow this way; App. E
+/* One flow: one section (or one bubble-filling chunk) moved from one rank
+ * to another (Sec. 4.1's unit of transfer; App. E
  * adds NVLink flows between the GPUs of one server).  A step is one
  * destination write: a reduce step with several sources has one flow per
  * source, all with the same step index. */

@@ -2,8 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-All times are in the paper's bandwidth-bound unit: a healthy NIC moves one
-element per time unit, a NIC with slowdown l moves one element in l units;
+All times are in the paper's bandwidth-bound unit, the time a healthy NIC
+needs for one element; a NIC slowed by a factor l needs l of these units;
 latency and launch costs are excluded (Sec. 3, problem setting).  Bandwidths
 are turned into slowdowns as l_i = max(b) / b_i, so ``Fraction`` keeps every
 value exact for the binary fractions used by the workloads.

@@ -3,11 +3,11 @@
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 Rules (paper: "Don't Let a Few Network Failures Slow the Entire AllReduce"):
-* Sec. 3 model: a healthy NIC moves one element per time unit, a NIC with
-  slowdown l one element per l units; App. B.1 time weighting: a transfer that
+* Sec. 3 model: the unit of time is what a healthy NIC takes per element;
+  a NIC slowed by l takes l units per element; App. B.1 time weighting: a transfer that
   touches a slow NIC costs the slow rate on both ends, so a flow of len
   elements between ranks a and b lasts len * max(l_a, l_b).
-* Sec. 4.1: each NIC receives at most one flow at a time; Sec. 4.2: no NIC
+* Sec. 4.1: a NIC takes in only one flow at once; Sec. 4.2: no NIC
   sends or receives two flows at once; the straggler sends and receives at
   the same time (full duplex).  So every rank has one send and one receive
   port, each busy with at most one flow.
