@@ -26,11 +26,11 @@
  * Pins (tests outside this file): exact int32 sums against the definition of
  * the result; contributor sets (nobody counted twice, everybody counted);
  * the fp error bound of recursive summation; a chain's association order
- * against a sequential cumulative sum; flow counts and split sizes against
- * the paper's worked examples; the lemmas' traffic volumes.  The exact
- * fp32/bf16 bit patterns follow from the readings above, which the paper
- * does not fix: parity unpinned by the paper for those bit patterns beyond
- * the properties listed.
+ * against a sequential cumulative sum, for every plan kind; flow counts and
+ * split sizes against the paper's worked examples; the lemmas' traffic
+ * volumes.  The paper does not fix the order of the additions, so the exact
+ * fp32/bf16 bit patterns follow from the readings above; given them, the
+ * cumulative-sum pins fix every fp32 bit.
  *
  * Source of every rule below (paper: "Don't Let a Few Network Failures Slow
  * the Entire AllReduce"):

@@ -8,7 +8,9 @@ properties the paper fixes reject it: every rank ends with the exact int32
 sum (Sec. 3), and the bubble-filling split of the Sec. 4.2 / App. C example
 (golden fixture) with App. C's D rounded to the nearest whole quantum at
 other lengths.  The unmodified copy passes the same checks, so the checks
-are not failing for some other reason.
+are not failing for some other reason.  A second set plants mistakes in
+the order of the additions, which exact sums cannot see, and requires the
+bit-for-bit comparison with the closed form of the readings to reject them.
 """
 import json
 import os
@@ -124,6 +126,78 @@ def test_planted_mistake_is_caught(tmp_path, monkeypatch, source, name, old, new
     assert source.count(old) == 1, f"mutation site of {name!r} not found once"
     so = _build(tmp_path, "m" + str(abs(hash(name)) % 10**8), source.replace(old, new))
     assert not _checks_with(monkeypatch, so), f"{name}: not caught"
+
+
+# ------------------------------------------------------- order of additions
+# Planted mistakes that keep every sum exact in int32 but add in another
+# order or round elsewhere: the exact sums cannot see them, the bit-for-bit
+# comparison with the closed form of the readings (oracle/closed_form.py,
+# tests/test_oracle_closed_form.py) must.
+ASSOCIATION_MUTATIONS = [
+    ("fp32 sources summed from the last",
+     "float acc = b[st->dst][c];\n    for (int i = 0; i < st->nsrc; ++i) acc = acc + b[srcs[i]][c];",
+     "float acc = b[st->dst][c];\n    for (int i = st->nsrc - 1; i >= 0; --i) acc = acc + b[srcs[i]][c];"),
+    ("stragglers folded best first",
+     "for (int i = 0; i < m; ++i) pre[npre++] = s->strag[i];",
+     "for (int i = m - 1; i >= 0; --i) pre[npre++] = s->strag[i];"),
+    ("bf16 rounded after every source",
+     "for (int i = 0; i < st->nsrc; ++i) acc = acc + bf16_widen(b[srcs[i]][c]);",
+     "for (int i = 0; i < st->nsrc; ++i) acc = bf16_widen(bf16_narrow(acc + bf16_widen(b[srcs[i]][c])));"),
+    ("local ring the other way round",
+     "return sv * s->g + (part + d) % s->g;",
+     "return sv * s->g + (part + s->g - d) % s->g;"),
+]
+
+# ring; one straggler with l >= 2 and with l < 2 (P2P chunks); two and three
+# stragglers; servers of 3 and 4 GPUs
+ORDER_PROFILES = [(6, [1.0] * 6, 4), (5, [0.5, 1, 1, 1, 1], 8), (8, [1.0] * 7 + [0.875], 8),
+                  (6, [0.5, 1, 1, 1, 1, 0.75], 8), (9, [0.875, 1, 1, 0.75, 1, 1, 1, 1, 0.5], 8)]
+ORDER_SERVERS = [(4, 3, [1, 1, 0.5, 1], 24), (3, 4, [1, 0.25, 1], 24)]
+
+
+def _closed_form_failures():
+    """Profiles whose fp32 or bf16 results differ from the closed form."""
+    from oracle import closed_form as cf
+    bad = []
+    for dtype in ("f32", "bf16"):
+        for p, bw, k in ORDER_PROFILES:
+            n = 64 * 3 * k * p + 17
+            x = np.random.default_rng(p + k).standard_normal((p, n)).astype(np.float32)
+            x = x if dtype == "f32" else oracle.bf16_round(x)
+            got = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x.copy())
+            if not np.array_equal(got[0].view(np.uint8), cf.final_values(dtype, x, bw, k).view(np.uint8)):
+                bad.append((dtype, p, bw))
+        for q, g, bw, k in ORDER_SERVERS:
+            n = 64 * 2 * k * g + 33
+            x = np.random.default_rng(q * g).standard_normal((q * g, n)).astype(np.float32)
+            x = x if dtype == "f32" else oracle.bf16_round(x)
+            got = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy())
+            want = cf.final_values_servers(dtype, x, q, g, bw, k)
+            if not np.array_equal(got[0].view(np.uint8), want.view(np.uint8)):
+                bad.append((dtype, q, g, bw))
+    return bad
+
+
+def _order_checks_with(monkeypatch, so):
+    """(exact int32 sums hold, closed-form failures) for the library `so`."""
+    monkeypatch.setattr(oracle, "_LIB", so)
+    monkeypatch.setattr(oracle, "_lib", None)
+    return _int32_sums_hold(), _closed_form_failures()
+
+
+def test_unmodified_copy_passes_the_order_pins(tmp_path, monkeypatch, source):
+    ints, bad = _order_checks_with(monkeypatch, _build(tmp_path, "control_order", source))
+    assert ints and bad == []
+
+
+@pytest.mark.parametrize("name,old,new", ASSOCIATION_MUTATIONS,
+                         ids=[m[0] for m in ASSOCIATION_MUTATIONS])
+def test_planted_order_mistake_is_caught(tmp_path, monkeypatch, source, name, old, new):
+    assert source.count(old) == 1, f"mutation site of {name!r} not found once"
+    so = _build(tmp_path, "o" + str(abs(hash(name)) % 10**8), source.replace(old, new))
+    ints, bad = _order_checks_with(monkeypatch, so)
+    assert ints, f"{name}: the exact int32 sums should not see this mistake"
+    assert bad, f"{name}: not caught"
 
 
 # ---------------------------------------------------------------- time model

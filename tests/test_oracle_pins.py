@@ -191,24 +191,91 @@ def test_f16_conversions_match_library():
     assert (oracle.f16_round(x) == ref).all()
 
 
-def test_fp32_association_is_the_chain(orc):
-    """Reading of the stage order (ordering 1: S1 chain from R[j], then the
-    straggler; ordering 2: straggler folded in at R[j] first): the fp32 result
-    equals numpy's sequential cumulative sum over the ranks in that order."""
-    p, n, k = 5, 64 * 8, 4
-    s = orc.Schedule(p, _bw(p, {2: 0.5}), n, k)
-    x = _rand("f32", p, n, 5)
-    y = orc.run(s, "f32", x.copy())
-    ring = list(s.ring)
+def _fold(vals):
+    """Left fold of fp32 additions in the listed order: numpy's sequential
+    cumulative sum (every step of the schedule adds one new value to a
+    running partial, and fp32 addition is commutative, so each result is such
+    a fold)."""
+    return np.cumsum(np.stack(vals), axis=0, dtype=np.float32)[-1]
+
+
+def _section_ranges(s):
+    out = {}
     for st in s.steps():
-        if st["slot"] != 1 or st["dst"] != ring[(st["sec"] + 1) % 4]:
-            continue
-        j, seg = st["sec"], st["seg"]
-        c = slice(st["off"], st["off"] + st["len"])
-        chain = [ring[(j + t) % 4] for t in range(4)]
-        order = chain + [2] if seg % 2 == 0 else [chain[0], 2] + chain[1:]
-        want = np.cumsum(x[order, c], axis=0, dtype=np.float32)[-1]
-        assert (y[0, c] == want).all()
+        out.setdefault((st["seg"], st["sec"]), (st["off"], st["len"]))
+    return out
+
+
+@pytest.mark.parametrize("p,slow,k", [(6, {}, 4), (5, {2: 0.5}, 4), (8, {1: 0.875}, 8),
+                                      (6, {0: 0.5, 5: 0.75}, 8),
+                                      (9, {0: 0.875, 3: 0.75, 8: 0.5}, 8)])
+def test_fp32_association_is_the_chain(orc, p, slow, k):
+    """Where the stage order puts each addition (Sec. 4.1 orderings, App. C
+    star, App. D folds; readings of where the stragglers' values join): the
+    fp32 result on every rank equals numpy's sequential cumulative sum over
+    the ranks in that order.  Ordering 1: chain from R[j], the worst
+    straggler last (the other stragglers first, at R[j], for A'/C');
+    ordering 2: every straggler, worst first, at R[j] before the chain; P2P
+    chunk: the straggler, then R[0..P'-1]."""
+    bw = _bw(p, slow)
+    n = 64 * 3 * k * p + 17
+    s = orc.Schedule(p, bw, n, k)
+    x = _rand("f32", p, n, 5 + p)
+    y = orc.run(s, "f32", x.copy())
+    ring, strag, pp = list(s.ring), list(s.stragglers), s.pp
+    m = len(strag)
+    seen = 0
+    for (seg, j), (off, ln) in _section_ranges(s).items():
+        c = slice(off, off + ln)
+        seen += ln
+        if j < 0:
+            order = strag[:1] + ring
+        else:
+            chain = [ring[(j + t) % pp] for t in range(pp)]
+            if m <= 1:
+                ordering = 1 if seg % 4 in (0, 2) else 2
+            else:
+                ordering = 2 if seg % 4 in (0, 1) else 1
+            if ordering == 2:
+                order = chain[:1] + strag + chain[1:]
+            else:
+                order = chain[:1] + strag[1:] + chain[1:] + strag[:1]
+        want = _fold([x[r, c] for r in order])
+        assert all((y[r, c].view(np.uint32) == want.view(np.uint32)).all() for r in range(p))
+    assert seen == n
+
+
+@pytest.mark.parametrize("q,g,slow", [(4, 3, {2: 0.5}), (3, 4, {1: 0.25}), (5, 2, {0: 0.75})])
+def test_fp32_association_servers(orc, q, g, slow):
+    """App. E: a server's value is the fold of its local ring from position
+    g-1 down to the leader; the chain folds the collected values; type 2
+    starts it with the straggler server's collected value, type 1 hands the
+    healthy sum to the straggler's leader and folds forward along its ring
+    (numpy's sequential cumulative sums)."""
+    k = 24
+    n = 64 * 2 * k * g + 33
+    s = orc.Schedule.servers(q, g, _sbw(q, slow), n, k)
+    x = _rand("f32", s.p, n, 9 + q * g)
+    y = orc.run(s, "f32", x.copy())
+    ring, sv, pp = list(s.ring), int(s.stragglers[0]), s.pp
+
+    def rank(server, part, d):
+        return server * g + (part + d) % g
+
+    seen = 0
+    for (seg, j), (off, ln) in _section_ranges(s).items():
+        c = slice(off, off + ln)
+        seen += ln
+        part, cseg = divmod(seg, k)
+        collect = [_fold([x[rank(h, part, d), c] for d in range(g - 1, -1, -1)])
+                   for h in [ring[(j + t) % pp] for t in range(pp)]]
+        if cseg % 4 in (0, 2):  # type 1
+            want = _fold([_fold(collect)] + [x[rank(sv, part, d), c] for d in range(g)])
+        else:
+            straggler = _fold([x[rank(sv, part, d), c] for d in range(g - 1, -1, -1)])
+            want = _fold(collect[:1] + [straggler] + collect[1:])
+        assert all((y[r, c].view(np.uint32) == want.view(np.uint32)).all() for r in range(s.p))
+    assert seen == n
 
 
 # ------------------------------------------------------------- stage pins
