@@ -658,6 +658,66 @@ def test_random_plans_bit_exact(o):
         assert bits_equal(to_host(d, c["dtype"]), ref), i
 
 
+def _random_rule_case(rng, i):
+    """A random plan at the sizes where the launch rules change: short
+    chains (3-8 healthy ranks) with 16 MiB to 512 MiB of rank buffers, where
+    32-bit types run one vector per lane in pipelined tiles; long chains
+    (33-200 ranks) with more tiles than one round of resident workgroups,
+    where they take per-XCD tile runs; server plans of the same sizes."""
+    def bandwidth():
+        return float(rng.integers(1, 8)) / 8 if rng.random() < 0.5 else float(rng.uniform(0.2, 0.999))
+    kind = ("short", "long", "servers")[i % 3]
+    if kind == "servers":
+        q, g = int(rng.integers(3, 17)), int(rng.choice([2, 4, 8]))
+        bw = [1.0] * q
+        bw[int(rng.integers(q))] = bandwidth()
+        n = int(rng.integers(1 << 19, (1 << 28) // (q * g)))
+        dtype = ["f32", "bf16", "i32"][int(rng.integers(3))]
+        return dict(servers=(q, g), p=q * g, bw=bw, n=n, k=8 * int(rng.integers(3, 9)), dtype=dtype)
+    if kind == "short":
+        p = int(rng.integers(4, 10))
+        m = min(int(rng.choice([0, 1, 1, 2])), p - 3)
+        n = int(rng.integers((4 << 20) // p, (128 << 20) // p))
+        dtype = ["f32", "i32", "f32", "bf16"][int(rng.integers(4))]
+    else:
+        p = int(rng.integers(33, 201))
+        m = int(rng.choice([0, 1, 2, 3]))
+        n = int(rng.integers(600_000, (1 << 28) // p))
+        dtype = ["f32", "i32", "bf16"][int(rng.integers(3))]
+    bw = [1.0] * p
+    for r in rng.choice(p, size=m, replace=False):
+        bw[int(r)] = bandwidth()
+    return dict(servers=None, p=p, bw=bw, n=n, k=4 * int(rng.integers(2, 33)), dtype=dtype)
+
+
+def test_random_plans_at_rule_sizes(o):
+    """18 seeded random plans at mid and large sizes (up to 2^28 elements in
+    all), each bit for bit against the oracle's full serial run on every
+    element of every rank."""
+    rng = np.random.default_rng(1680)
+    for i in range(18):
+        c = _random_rule_case(rng, i)
+        _say(f"case rule-size random #{i}: p={c['p']} n={c['n']} k={c['k']} "
+             f"dtype={c['dtype']} servers={c['servers']} bw={sorted(set(c['bw']))}")
+        if c["servers"] is None:
+            pl = o.optcc_plan(c["p"], c["bw"], c["n"], c["k"])
+            sched = oracle.Schedule(c["p"], c["bw"], c["n"], c["k"])
+        else:
+            q, g = c["servers"]
+            pl = o.optcc_plan_servers(q, g, c["bw"], c["n"], c["k"])
+            sched = oracle.Schedule.servers(q, g, c["bw"], c["n"], c["k"])
+        x = rand_inputs(c["dtype"], c["p"], c["n"], 7000 + i)
+        d = to_device(x, c["dtype"])
+        o.optcc_allreduce_emulate(d, c["p"], c["n"], c["dtype"], pl)
+        torch.cuda.synchronize()
+        got = to_host(d, c["dtype"])
+        del d
+        ref = oracle.run(sched, c["dtype"], x)
+        assert bits_equal(got, ref), i
+        del x, got, ref
+        torch.cuda.empty_cache()
+
+
 def test_one_graph_of_several_allreduces(o):
     """Several AllReduces with different plans and element types (bubble
     filling, several stragglers, a 40-rank chain launched at one workgroup
