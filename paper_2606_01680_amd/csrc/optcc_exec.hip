@@ -20,10 +20,6 @@ namespace {
 
 using namespace kern;
 
-// The plan's tables for tiles of tile_elems elements on the current device,
-// uploaded on first use and cached.  The upload (hipMalloc, hipMemcpy) may
-// not run while `stream` is being captured into a graph: such a first call
-// fails before touching the device, and the capture stays valid.
 // The plan's host tile table for tiles of tile_elems elements: tile_elems-
 // element pieces of every segment's ring part and P2P chunk, built once per
 // tile length.  The caller holds pl.mu; the vector lives as long as the plan.
@@ -60,6 +56,10 @@ int64_t tile_count(const optcc_plan_t &pl, int tile_elems) {
   return t;
 }
 
+// The plan's tables for tiles of tile_elems elements on the current device,
+// uploaded on first use and cached.  The upload (hipMalloc, hipMemcpy) may
+// not run while `stream` is being captured into a graph: such a first call
+// fails before touching the device, and the capture stays valid.
 int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, DeviceTables *out) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
