@@ -199,15 +199,47 @@ def cpu_leg(w, x0, plan, traffic_bytes, budget_s, threads):
                       f"{how}, mean of {len(times)} run(s) of {t:.3f} s"}
 
 
+def brute_leg(w, x0, budget_s):
+    """The definition of the result timed on the host: every coordinate's
+    sum over the ranks in fp64 (int64 wrapped to int32), numpy, on leading
+    coordinates of the workload (whole vector if it fits the budget).  The
+    rate counts the input bytes it reads."""
+    import numpy as np
+    import oracle
+
+    def run(end):
+        src = x0[:, :end].cpu()
+        if w.dtype in ("bf16", "f16"):
+            import torch
+            host = src.view(torch.int16).numpy().view(np.uint16)
+        else:
+            host = src.numpy()
+        t = time.perf_counter()
+        oracle.brute_sum(w.dtype, host)
+        return time.perf_counter() - t
+
+    end = min(w.n, 1 << 16)
+    t = run(end)
+    end = int(min(w.n, max(end, end * budget_s / max(t, 1e-6))))
+    t = run(end)
+    in_bytes = w.p * end * (2 if w.dtype in ("bf16", "f16") else 4)
+    return {"value": round(in_bytes / t / 1e9, 4), "unit": "GB/s of input read", "cores": 1,
+            "seconds": round(t, 4),
+            "sample": f"first {end} of {w.n} elements per rank, all {w.p} ranks",
+            "kind": "brute force: fp64 (int64 for int32) sum over the ranks, numpy "
+                    "(the definition of the result, not the schedule)"}
+
+
 def cpu_baseline(w, x0, plan, traffic_bytes, serial_s, parallel_s):
     """Two legs: the serial oracle on one core, and the same executor on all
-    the cores this process may use."""
+    the cores this process may use; beside them the brute-force sum."""
     serial = cpu_leg(w, x0, plan, traffic_bytes, serial_s, 1)
     threads = oracle_threads()
     par = cpu_leg(w, x0, plan, traffic_bytes, parallel_s, threads)
     out = dict(serial)
     out["kind"] = "oracle"
     out["all_cores"] = dict(par, kind="oracle, OpenMP over segments (bit-identical to serial)")
+    out["brute_force"] = brute_leg(w, x0, min(2.0, parallel_s))
     out.update(host_info())
     return out
 
@@ -336,6 +368,12 @@ def measure(torch, optcc, w, args, check=True):
         result = full_check(torch, w, x, x0)
     del x
 
+    # torch's device copy of as many bytes as the rank buffers hold, timed
+    # in the same run: a reference rate of one read and one write stream
+    buf_bytes = w.p * w.n * (2 if w.dtype in ("bf16", "f16") else 4)
+    copy_ms, copy_gbps = copy_rate(torch, buf_bytes, max(args.steps, 5), 2)
+    torch.cuda.empty_cache()
+
     achieved = alg_bytes / (ms_launch * 1e-3) / 1e9
     # counter traffic was taken at the workload's own N
     traffic = measured_traffic(w.name, args.launches) if args.n is None else None
@@ -361,6 +399,13 @@ def measure(torch, optcc, w, args, check=True):
             "kernel_ms": round(ms_launch, 5),
             "kernel_ms_median": round(statistics.median(launch_ms), 5),
             "kernel_ms_min": round(min(launch_ms), 5), "kernel": "optcc_exec_kernel",
+        },
+        "copy_reference": {
+            "kernel": "torch copy_ (the runtime's blit kernel)", "bytes": buf_bytes,
+            "ms": round(copy_ms, 5), "GBps_read_plus_write": round(copy_gbps, 2),
+            "achieved_over_copy": round(achieved / copy_gbps, 4),
+            "traffic_over_copy": None if traffic is None else round(
+                traffic / (ms_launch * 1e-3) / 1e9 / copy_gbps, 4),
         },
         "model_time_over_N": model_times(optcc, w, plan),
         "check": result,
@@ -505,6 +550,7 @@ def main():
             "launches_per_step": rec["launches_per_step"], "plan_kind": plan.kind,
         },
         "roofline": rec["roofline"],
+        "copy_reference": rec["copy_reference"],
         "model_time_over_N": times,
         # the same model times in seconds for this message on healthy
         # 200 Gb/s NICs (25 GB/s, the paper's ConnectX-6 HDR setting)
@@ -528,7 +574,8 @@ def main():
                 r = {k: v for k, v in rec.items() if k not in ("executor_launches", "stages")}
                 if cpu is not None:
                     r["cpu_baseline"] = {"serial": {k: cpu[k] for k in ("value", "cores", "sample")},
-                                         "all_cores": cpu["all_cores"]}
+                                         "all_cores": cpu["all_cores"],
+                                         "brute_force": cpu["brute_force"]}
                 configs[name] = r
                 continue
             print(f"bench: measuring {name}", file=sys.stderr, flush=True)
@@ -538,7 +585,8 @@ def main():
             if not args.no_cpu_baseline:
                 legs = args.cpu_seconds / 5
                 r["cpu_baseline"] = {"serial": cpu_leg(wc, xc, pc, bc, legs, 1),
-                                     "all_cores": cpu_leg(wc, xc, pc, bc, legs, oracle_threads())}
+                                     "all_cores": cpu_leg(wc, xc, pc, bc, legs, oracle_threads()),
+                                     "brute_force": brute_leg(wc, xc, min(1.0, legs))}
             del xc
             torch.cuda.empty_cache()
             failed |= r["check"] == "FAIL"
