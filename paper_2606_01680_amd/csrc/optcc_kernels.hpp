@@ -148,8 +148,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // against the LDS wait counter too, so every wait for an LDS pointer read
 // also waits for the loads in flight.  Global (GA) accesses keep the two
 // counters apart.  Measured: the server lane is 2 % faster with global
-// accesses (q32g4_f32), the one-GPU-per-server lanes 1.7 % faster with
-// generic ones (p128_f32), equal at p = 8.
+// accesses (q32g4_f32).  The one-GPU-per-server lanes gain at most 2 % from
+// them at any message size (p = 4 to 128, 2^18 to 2^26 elements per rank;
+// full-size workloads within 0.3 %): the waves of a CU keep enough loads in
+// flight either way, so those lanes keep generic pointers.
 template <class T, bool GA>
 using MemPtr = typename std::conditional<GA, __attribute__((address_space(1))) T *, T *>::type;
 
