@@ -79,14 +79,21 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, De
   DeviceTables d;
   const size_t sb = pl.segdesc.size() * sizeof(SegDesc);
   const size_t tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
+  const size_t wb = (size_t)kStealSlots * kStealWords * sizeof(uint32_t);
   err = hipMalloc(&d.segs, sb);
   if (err == hipSuccess) err = hipMalloc(&d.tiles, tb);
+  if (err == hipSuccess) err = hipMalloc(&d.steal, wb);
   if (err == hipSuccess) err = hipMemcpy(d.segs, pl.segdesc.data(), sb, hipMemcpyHostToDevice);
   if (err == hipSuccess && !tiles.empty())
     err = hipMemcpy(d.tiles, tiles.data(), tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice);
+  if (err == hipSuccess) {  // zero counters, in place before this call returns (like the tables)
+    const std::vector<uint32_t> zero((size_t)kStealSlots * kStealWords, 0u);
+    err = hipMemcpy(d.steal, zero.data(), wb, hipMemcpyHostToDevice);
+  }
   if (err != hipSuccess) {
     if (d.segs) (void)hipFree(d.segs);
     if (d.tiles) (void)hipFree(d.tiles);
+    if (d.steal) (void)hipFree(d.steal);
     return fail(err == hipErrorOutOfMemory ? OPTCC_ENOMEM : OPTCC_EDEVICE,
                 std::string("uploading plan tables: ") + hipGetErrorString(err));
   }
@@ -350,6 +357,31 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     runs = resident <= 0 || ntiles > resident;
   }
   a.xcd_runs = runs ? 1 : 0;
+  // Work stealing for the same long chains at one workgroup per CU when
+  // their tiles take the identity order (more than kXcdRunsMaxTiles): a
+  // grid of the resident workgroups takes tiles from a device counter.  The
+  // eight XCDs do not run equally fast (per-wave timestamps of p128_f32:
+  // XCDs 1, 3, 5, 7 spend about 5 % longer per tile than 0, 2, 4, 6), and
+  // with one eighth of the tiles each the fast ones wait at the end.
+  // Measured (back-to-back calls, results bit for bit equal): p = 128 fp32
+  // at 2^23 / 2^24 / 2^25 elements per rank 2.1 / 4.2 / 3.6 % faster, p = 64
+  // 3.4 / 2.2 / 2.5 %, int32 p = 128 at 2^24 2.6 %, one straggler at 0.875
+  // with p = 96 (P2P chunks) 2.9 %, p = 40 and 48 1.5-3.2 %; bf16 (full
+  // occupancy) 7.6 % slower, and with per-XCD runs (fewer tiles) it gains
+  // nothing, so neither takes it.  Not under graph capture: a captured
+  // launch keeps its counter block, and replays of the graph on two streams
+  // at once would share it; the no-allocation entry point keeps the static
+  // order too.
+  bool steal = long_chain && !servers && a.occ_lds > 0 && !runs && !noalloc;
+  int steal_grid = 0;
+  if (steal) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    steal = hipStreamIsCapturing(st, &cap) == hipSuccess && cap == hipStreamCaptureStatusNone;
+  }
+  if (steal) {
+    steal_grid = resident_workgroups(a, dtype, servers, vec16, two_vec);
+    steal = steal_grid > 0 && steal_grid < ntiles;
+  }
   DeviceTables dt;
   int rc = noalloc ? scratch_tables(*pl, tile_elems, st, &dt)
                    : device_tables(*pl, tile_elems, st, &dt);
@@ -357,6 +389,13 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   a.tiles = dt.tiles;
   a.segs = dt.segs;
   a.ntiles = dt.ntiles;
+  if (steal && dt.steal) {
+    // one counter block per launch, round robin over kStealSlots: launches
+    // in flight at once (any streams) use different blocks
+    const uint32_t slot = pl->steal_next.fetch_add(1u, std::memory_order_relaxed) % kStealSlots;
+    a.steal = dt.steal + (size_t)slot * kStealWords;
+    a.grid = steal_grid;
+  }
   const int nl = launches == 1 ? 1 : se - sb;
   for (int l = 0; l < nl; ++l) {
     a.sb = launches == 1 ? sb : sb + l;
@@ -408,6 +447,7 @@ extern "C" void optcc_plan_free(optcc_plan_t *pl) {
       if (have_dev) (void)hipSetDevice(kv.first.first);
       (void)hipFree(kv.second.segs);
       (void)hipFree(kv.second.tiles);
+      (void)hipFree(kv.second.steal);
     }
     if (have_dev && !pl->dev.empty()) (void)hipSetDevice(cur);
     pl->dev.clear();

@@ -1,6 +1,7 @@
 // Internal definitions shared by the host planner and the GPU executor.
 #pragma once
 
+#include <atomic>
 #include <cstdint>
 #include <map>
 #include <mutex>
@@ -51,9 +52,15 @@ constexpr int64_t kTileMinBytes2 = 72 << 10;
 // while the launch would have fewer than this many tiles.
 constexpr int64_t kTileMinCount = 1024;
 
+// Counter blocks of work-stealing launches (kStealWords words each, one
+// block per launch, taken round robin from kStealSlots per table).
+constexpr int kStealSlots = 4096;
+constexpr int kStealWords = 16;  // 64 bytes: blocks of concurrent launches share no cache line
+
 struct DeviceTables {
   SegDesc *segs = nullptr;
   TileDesc *tiles = nullptr;
+  uint32_t *steal = nullptr;  // kStealSlots blocks, zero between launches
   int64_t ntiles = 0;
 };
 
@@ -84,6 +91,8 @@ struct optcc_plan {
   mutable std::map<std::pair<int, int>, optcc::DeviceTables> dev;  // (device, tile elements)
   // host tile tables per tile length (the source of the device copies)
   mutable std::map<int, std::vector<optcc::TileDesc>> host_tiles;
+  // next counter block for a work-stealing launch (round robin)
+  mutable std::atomic<uint32_t> steal_next{0};
 };
 
 namespace optcc {

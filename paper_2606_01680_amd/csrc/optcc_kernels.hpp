@@ -86,6 +86,12 @@ struct KArgs {
   // per lane defer each vector's Stage 4 stores into the next vector's
   // Stage 1 chain (pipelined_ring_tile)
   int32_t pipe;
+  // launch setting, not read by the kernel: workgroups to launch (0: one
+  // per tile)
+  int32_t grid;
+  // work stealing when not NULL: [0] the next tile, [1] workgroups that have
+  // finished; both zero at launch and reset to zero by the last workgroup
+  uint32_t *steal;
   // rank pointers.  g = 1: [0, pp) healthy ranks in ring order, [pp, pp+m)
   // stragglers sorted by slowdown (worst first).  g > 1: [h*g, h*g+g) the g
   // GPUs (by local index) of the h-th healthy server in ring order, then the
@@ -848,69 +854,99 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
   }
 }
 
-// W elements per lane access: 16 bytes when every rank buffer is 16-byte
-// aligned, else 1 element.  A lane takes L such vectors of a tile
-// at a stride of one workgroup-width, in lockstep; vectors past the tile's
-// last whole group go one at a time, and elements past the last whole vector
-// (only at the end of the rank vectors) one by one.
-//
+// One tile: every step of the schedule on its elements.  W elements per
+// lane access: 16 bytes when every rank buffer is 16-byte aligned, else 1
+// element.  A lane takes L such vectors of the tile at a stride of one
+// workgroup-width, in lockstep; vectors past the tile's last whole group go
+// one at a time, and elements past the last whole vector (only at the end
+// of the rank vectors) one by one.
+template <class D, int W, int L, bool S, int G>
+__device__ __forceinline__ void run_tile(const KArgs &a, void *const *rp, int64_t t) {
+  constexpr int B = kHopWindow;
+  constexpr int64_t kStride = (int64_t)kThreads * W;
+  const TileDesc td = a.tiles[t];
+  const bool p2p = td.meta & 1;
+  const SegDesc sd = a.segs[td.meta >> 1];
+  const int64_t end = td.begin + td.len;
+  int64_t e0 = td.begin + (int64_t)threadIdx.x * W;
+  if constexpr (!S && L == 1) {
+    if (a.pipe && !p2p && a.sb == 0 && a.se == OPTCC_NUM_SLOTS) {
+      pipelined_ring_tile<D, W, B>(a, rp, sd, e0, end, kStride);
+      int64_t x = e0 + (end - W - e0 >= 0 ? ((end - W - e0) / kStride + 1) * kStride : 0);
+      for (; x < end; x += kStride)
+        for (int64_t y = x; y < end && y < x + W; ++y) {
+          const int64_t e[1] = {y};
+          run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
+        }
+      return;
+    }
+  }
+  for (; e0 + (L - 1) * kStride + W <= end; e0 += L * kStride) {
+    int64_t e[L];
+#pragma unroll
+    for (int l = 0; l < L; ++l) e[l] = e0 + l * kStride;
+    run_elems<D, W, L, B, S, G>(a, rp, sd, p2p, e);
+  }
+  for (; e0 < end; e0 += kStride) {
+    if (e0 + W <= end) {
+      const int64_t e[1] = {e0};
+      run_elems<D, W, 1, B, S, G>(a, rp, sd, p2p, e);
+    } else {
+      for (int64_t x = e0; x < end; ++x) {
+        const int64_t e[1] = {x};
+        run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
+      }
+    }
+  }
+}
+
 // S selects the several-GPUs-per-server lane (App. E); its plans have no
 // point-to-point chunks.  G: GPUs per server when fixed at compile time
 // (0: read from the arguments).
 template <class D, int W, int L, bool S, int G>
 __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
-  constexpr int B = kHopWindow;
-  constexpr int64_t kStride = (int64_t)kThreads * W;
   __shared__ void *rp[kMaxRanks];
   const int nrp = S ? (a.pp + 1) * a.g : a.pp;  // pointers the lanes index from LDS
   for (int i = threadIdx.x; i < nrp; i += kThreads) rp[i] = a.ptr[i];
   __syncthreads();
-  // Workgroups are dealt to the XCDs round robin by workgroup index.  With
-  // xcd_runs, workgroup t0 takes tile (t0 mod X) * per + t0 / X, so each XCD
-  // sweeps its own contiguous run of tiles.  Any XCD count keeps every tile
-  // covered exactly once; X = 8 matches MI355X.
+  if (a.steal) {
+    // Work stealing: a grid of at most the resident workgroups takes tiles
+    // in order from one device counter, so the CUs and XCDs that run ahead
+    // take more of them.  Every workgroup leaves once the counter has passed
+    // the last tile; the last one to leave resets the counters for the next
+    // launch that uses them.
+    __shared__ int64_t next;
+    for (;;) {
+      if (threadIdx.x == 0) {
+        const uint32_t i = atomicAdd(&a.steal[0], 1u);
+        next = (int64_t)i < a.ntiles ? (int64_t)i : -1;
+      }
+      __syncthreads();
+      const int64_t t = next;
+      __syncthreads();
+      if (t < 0) break;
+      run_tile<D, W, L, S, G>(a, rp, t);
+    }
+    if (threadIdx.x == 0) {
+      __threadfence();
+      if (atomicAdd(&a.steal[1], 1u) == gridDim.x - 1) {
+        __threadfence();
+        atomicExch(&a.steal[0], 0u);
+        atomicExch(&a.steal[1], 0u);
+      }
+    }
+    return;
+  }
+  // Static order.  Workgroups are dealt to the XCDs round robin by workgroup
+  // index.  With xcd_runs, workgroup t0 takes tile (t0 mod X) * per + t0 / X,
+  // so each XCD sweeps its own contiguous run of tiles.  Any XCD count keeps
+  // every tile covered exactly once; X = 8 matches MI355X.
   constexpr int64_t kXcds = 8;
   const int64_t per = (a.ntiles + kXcds - 1) / kXcds;
   const int64_t cover = a.xcd_runs ? per * kXcds : a.ntiles;
   for (int64_t t0 = blockIdx.x; t0 < cover; t0 += gridDim.x) {
     const int64_t t = a.xcd_runs ? (t0 % kXcds) * per + t0 / kXcds : t0;
-    if (t >= a.ntiles) continue;
-    const TileDesc td = a.tiles[t];
-    const bool p2p = td.meta & 1;
-    const SegDesc sd = a.segs[td.meta >> 1];
-    const int64_t end = td.begin + td.len;
-    int64_t e0 = td.begin + (int64_t)threadIdx.x * W;
-    if constexpr (!S && L == 1) {
-      if (a.pipe && !p2p && a.sb == 0 && a.se == OPTCC_NUM_SLOTS) {
-        pipelined_ring_tile<D, W, B>(a, rp, sd, e0, end, kStride);
-        // elements past the last whole vector (only at the end of the rank
-        // vectors) one by one
-        int64_t x = e0 + (end - W - e0 >= 0 ? ((end - W - e0) / kStride + 1) * kStride : 0);
-        for (; x < end; x += kStride)
-          for (int64_t y = x; y < end && y < x + W; ++y) {
-            const int64_t e[1] = {y};
-            run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
-          }
-        continue;
-      }
-    }
-    for (; e0 + (L - 1) * kStride + W <= end; e0 += L * kStride) {
-      int64_t e[L];
-#pragma unroll
-      for (int l = 0; l < L; ++l) e[l] = e0 + l * kStride;
-      run_elems<D, W, L, B, S, G>(a, rp, sd, p2p, e);
-    }
-    for (; e0 < end; e0 += kStride) {
-      if (e0 + W <= end) {
-        const int64_t e[1] = {e0};
-        run_elems<D, W, 1, B, S, G>(a, rp, sd, p2p, e);
-      } else {
-        for (int64_t x = e0; x < end; ++x) {
-          const int64_t e[1] = {x};
-          run_elems<D, 1, 1, B, S, G>(a, rp, sd, p2p, e);
-        }
-      }
-    }
+    if (t < a.ntiles) run_tile<D, W, L, S, G>(a, rp, t);
   }
 }
 

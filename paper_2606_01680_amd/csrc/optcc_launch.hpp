@@ -28,7 +28,7 @@ namespace kern {
 template <class D, bool S, int G>
 hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st, int *occ) {
   constexpr int W16 = 16 / (int)sizeof(typename D::S);
-  const int64_t grid64 = std::min<int64_t>(a.ntiles, (int64_t)1 << 30);
+  const int64_t grid64 = std::min<int64_t>(a.ntiles, a.grid > 0 ? (int64_t)a.grid : (int64_t)1 << 30);
   const dim3 grid((unsigned)std::max<int64_t>(grid64, 1)), block(kThreads);
   if constexpr (G == 0) {
     if (!vec16)  // element-aligned buffers: one element per access

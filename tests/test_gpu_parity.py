@@ -616,6 +616,127 @@ def test_threads_share_one_plan(o):
         assert bits_equal(to_host(devs[dt], dt), ref), dt
 
 
+# Long chains (more than 32 healthy ranks, one workgroup per CU) whose
+# tiles outnumber the per-XCD-run limit (2,048) run as a persistent grid
+# that takes tiles from a device counter (work stealing); bf16 keeps the
+# static order.  Sizes just above the limit, ragged.
+STEAL = [(40, {5: 0.6}, 2048 * 2100 + 77, 8), (70, {3: 0.875}, 2048 * 2200 + 130, 16),
+         (36, {}, 2048 * 2300 + 3, 4)]
+
+
+@pytest.mark.parametrize("p,slow,n,k", STEAL)
+def test_work_stealing_launches(o, p, slow, n, k):
+    """Three calls in a row of a work-stealing plan (the counters reset
+    themselves at the end of each launch), fp32, int32 and fp16: the first
+    result equals the oracle on every element, the others equal the first."""
+    bw = _bw(p, slow)
+    pl = o.optcc_plan(p, bw, n, k)
+    sched = oracle.Schedule(p, bw, n, k)
+    for dtype in ("f32", "i32", "f16"):
+        _say(f"case work stealing p={p} n={n} k={k} dtype={dtype}")
+        x = rand_inputs(dtype, p, n, 90 + p)
+        d = to_device(x, dtype)
+        d0 = d.clone()
+        first = None
+        for rep in range(3):
+            d.copy_(d0)
+            o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+            torch.cuda.synchronize()
+            if first is None:
+                first = d.clone()
+            else:
+                assert torch.equal(int_view(d), int_view(first)), rep
+        del d, d0
+        ref = oracle.run(sched, dtype, x)
+        assert bits_equal(to_host(first, dtype), ref), dtype
+        del first
+        torch.cuda.empty_cache()
+
+
+def test_work_stealing_equals_static_order(o):
+    """Work stealing changes only which workgroup runs which tile: the same
+    AllReduce through the no-allocation entry point and inside a captured
+    HIP graph (both keep the static tile order) gives the same bits."""
+    p, n, k = 40, 2048 * 2100 + 77, 8
+    bw = _bw(p, {5: 0.6})
+    pl = o.optcc_plan(p, bw, n, k)
+    x = rand_inputs("f32", p, n, 4242)
+    d0 = to_device(x, "f32")
+    d = d0.clone()
+    o.optcc_allreduce_emulate(d, p, n, "f32", pl)
+    torch.cuda.synchronize()
+    steal = d.clone()
+    d.copy_(d0)
+    o.optcc_allreduce_emulate_noalloc(d, p, n, "f32", pl)
+    torch.cuda.synchronize()
+    assert torch.equal(int_view(d), int_view(steal))
+    g = torch.cuda.CUDAGraph()
+    d.copy_(d0)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            o.optcc_allreduce_emulate(d, p, n, "f32", pl)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        _say(f"case work stealing against a captured graph, replay {rep}")
+        d.copy_(d0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(int_view(d), int_view(steal)), rep
+    del g
+
+
+def test_work_stealing_threads_share_one_plan(o):
+    """Four host threads, each on its own stream and buffers, run one
+    work-stealing plan at once, three times each: concurrent launches take
+    different counter blocks, and every result equals the oracle."""
+    import threading
+    p, n, k = 40, 2048 * 2100 + 77, 8
+    bw = _bw(p, {5: 0.6})
+    pl = o.optcc_plan(p, bw, n, k)
+    names = ["a", "b", "c", "d"]
+    dts = {"a": "f32", "b": "i32", "c": "f32", "d": "f16"}
+    xs = {nm: rand_inputs(dts[nm], p, n, 500 + i) for i, nm in enumerate(names)}
+    devs = {nm: to_device(xs[nm], dts[nm]) for nm in names}
+    orig = {nm: devs[nm].clone() for nm in names}
+    streams = {nm: torch.cuda.Stream() for nm in names}
+    o.optcc_allreduce_emulate(devs["a"].clone(), p, n, "f32", pl)  # tables uploaded first
+    torch.cuda.synchronize()
+    errors, out = [], {}
+    start = threading.Barrier(len(names))
+
+    def work(nm):
+        try:
+            start.wait()
+            with torch.cuda.stream(streams[nm]):
+                for it in range(3):
+                    d = devs[nm]
+                    d.copy_(orig[nm])
+                    o.optcc_allreduce_emulate(d, p, n, dts[nm], pl, stream=streams[nm])
+                    if it == 0:
+                        out[nm] = d.clone()
+                    elif not torch.equal(int_view(d), int_view(out[nm])):
+                        errors.append((nm, it, "differs from the first call"))
+                streams[nm].synchronize()
+        except Exception as e:  # reported by the main thread
+            errors.append((nm, e))
+
+    _say("case threads sharing one work-stealing plan")
+    ts = [threading.Thread(target=work, args=(nm,)) for nm in names]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    sched = oracle.Schedule(p, bw, n, k)
+    for nm in names:
+        ref = oracle.run(sched, dts[nm], xs[nm].copy())
+        assert bits_equal(to_host(out[nm], dts[nm]), ref), nm
+
+
 def _random_case(rng):
     """One random plan: ranks, stragglers and their bandwidths (NIC losses of
     eighths or any fraction), N, k, element type; a fifth are server plans."""
