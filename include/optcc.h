@@ -155,6 +155,16 @@ void optcc_plan_free(optcc_plan_t *plan);
  * that is N of about 2^39 elements per rank at k = 4, beyond one GPU's HBM),
  * OPTCC_EDEVICE, OPTCC_ENOMEM (first use of the plan on a device allocates
  * its tables).  These checks are made before any device call.
+ *
+ * Launch order of the tiles (never the result): plans of more than 32
+ * healthy ranks whose elements are not bf16 and whose tiles outnumber 2,048
+ * run a grid of the resident workgroups that take tiles from a device
+ * counter.  Each such call takes its own 64-byte counter block from a ring
+ * of 4,096 per plan and device (allocated and zeroed with the tables), and
+ * its last workgroup sets the block back to zero.  So at most 4,096 of
+ * these calls of one plan may be queued or running at once on one device,
+ * over all streams; beyond that two could share a block.  Calls captured
+ * into a HIP graph keep the static order.
  */
 int optcc_allreduce_emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
                             const optcc_plan_t *plan, void *stream);
@@ -208,7 +218,10 @@ int optcc_allreduce_emulate_slots(void *const *bufs, int p, int64_t N, optcc_dty
  * start at zero): calls on one GPU that overlap in time (on different
  * streams, or from several host threads without ordering) race and give
  * undefined results.  The plan must stay alive until the call's work on
- * `stream` has completed (its host tables are the copies' source).
+ * `stream` has completed (its host tables are the copies' source).  Tiles
+ * always run in the static order here (no device counters), so the long
+ * plans that optcc_allreduce_emulate runs with work stealing take a few per
+ * cent longer through this entry point; the result is the same.
  */
 #define OPTCC_NOALLOC_SCRATCH_BYTES (4 << 20)
 int optcc_allreduce_emulate_noalloc(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype,
