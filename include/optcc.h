@@ -160,7 +160,9 @@ void optcc_plan_free(optcc_plan_t *plan);
  * healthy ranks whose elements are not bf16 and whose tiles outnumber 2,048
  * run a grid of the resident workgroups that take tiles from a device
  * counter.  Each such call takes its own 64-byte counter block from a ring
- * of 4,096 per plan and device (allocated and zeroed with the tables), and
+ * of 4,096 per plan and device (256 KiB, allocated and zeroed by the plan's
+ * first such call on the device; if that fails the call keeps the static
+ * order), and
  * its last workgroup sets the block back to zero.  So at most 4,096 of
  * these calls of one plan may be queued or running at once on one device,
  * over all streams; beyond that two could share a block.  Calls captured

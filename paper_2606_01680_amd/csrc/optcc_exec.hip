@@ -79,21 +79,14 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, De
   DeviceTables d;
   const size_t sb = pl.segdesc.size() * sizeof(SegDesc);
   const size_t tb = std::max<size_t>(tiles.size(), 1) * sizeof(TileDesc);
-  const size_t wb = (size_t)kStealSlots * kStealWords * sizeof(uint32_t);
   err = hipMalloc(&d.segs, sb);
   if (err == hipSuccess) err = hipMalloc(&d.tiles, tb);
-  if (err == hipSuccess) err = hipMalloc(&d.steal, wb);
   if (err == hipSuccess) err = hipMemcpy(d.segs, pl.segdesc.data(), sb, hipMemcpyHostToDevice);
   if (err == hipSuccess && !tiles.empty())
     err = hipMemcpy(d.tiles, tiles.data(), tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice);
-  if (err == hipSuccess) {  // zero counters, in place before this call returns (like the tables)
-    const std::vector<uint32_t> zero((size_t)kStealSlots * kStealWords, 0u);
-    err = hipMemcpy(d.steal, zero.data(), wb, hipMemcpyHostToDevice);
-  }
   if (err != hipSuccess) {
     if (d.segs) (void)hipFree(d.segs);
     if (d.tiles) (void)hipFree(d.tiles);
-    if (d.steal) (void)hipFree(d.steal);
     return fail(err == hipErrorOutOfMemory ? OPTCC_ENOMEM : OPTCC_EDEVICE,
                 std::string("uploading plan tables: ") + hipGetErrorString(err));
   }
@@ -101,6 +94,33 @@ int device_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, De
   pl.dev[{dev, tile_elems}] = d;
   *out = d;
   return OPTCC_OK;
+}
+
+// The work-stealing counter blocks of the plan's tables for tiles of
+// tile_elems elements on the current device: kStealSlots blocks, allocated
+// and zeroed on the first launch that steals (never under capture: such
+// launches keep the static order).  NULL if they cannot be allocated; the
+// caller then keeps the static order, which gives the same result.
+uint32_t *steal_counters(const optcc_plan_t &pl, int tile_elems) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lk(pl.mu);
+  auto it = pl.dev.find({dev, tile_elems});
+  if (it == pl.dev.end()) return nullptr;
+  DeviceTables &d = it->second;
+  if (!d.steal) {
+    const size_t wb = (size_t)kStealSlots * kStealWords * sizeof(uint32_t);
+    uint32_t *c = nullptr;
+    if (hipMalloc(&c, wb) != hipSuccess) return nullptr;
+    // zeroed in place before this call returns, like the tables
+    const std::vector<uint32_t> zero((size_t)kStealSlots * kStealWords, 0u);
+    if (hipMemcpy(c, zero.data(), wb, hipMemcpyHostToDevice) != hipSuccess) {
+      (void)hipFree(c);
+      return nullptr;
+    }
+    d.steal = c;
+  }
+  return d.steal;
 }
 
 // Device memory of optcc_allreduce_emulate_noalloc: the plan's tables are
@@ -389,11 +409,12 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   a.tiles = dt.tiles;
   a.segs = dt.segs;
   a.ntiles = dt.ntiles;
-  if (steal && dt.steal) {
+  uint32_t *counters = steal ? steal_counters(*pl, tile_elems) : nullptr;
+  if (counters) {
     // one counter block per launch, round robin over kStealSlots: launches
     // in flight at once (any streams) use different blocks
     const uint32_t slot = pl->steal_next.fetch_add(1u, std::memory_order_relaxed) % kStealSlots;
-    a.steal = dt.steal + (size_t)slot * kStealWords;
+    a.steal = counters + (size_t)slot * kStealWords;
     a.grid = steal_grid;
   }
   const int nl = launches == 1 ? 1 : se - sb;

@@ -60,7 +60,7 @@ constexpr int kStealWords = 16;  // 64 bytes: blocks of concurrent launches shar
 struct DeviceTables {
   SegDesc *segs = nullptr;
   TileDesc *tiles = nullptr;
-  uint32_t *steal = nullptr;  // kStealSlots blocks, zero between launches
+  uint32_t *steal = nullptr;  // kStealSlots blocks, zero between launches (on first use)
   int64_t ntiles = 0;
 };
 
