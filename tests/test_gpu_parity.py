@@ -688,6 +688,34 @@ def test_work_stealing_equals_static_order(o):
     del g
 
 
+def test_work_stealing_slot_ranges(o):
+    """A work-stealing plan run as two slot ranges in a row, and as one
+    launch per slot (each launch takes the same counter block after the one
+    before has set it back to zero), equals the fused call bit for bit, and
+    the oracle's stage prefix after the first range."""
+    p, n, k = 40, 2048 * 2100 + 77, 8
+    bw = _bw(p, {5: 0.6})
+    pl = o.optcc_plan(p, bw, n, k)
+    x = rand_inputs("f32", p, n, 777)
+    d0 = to_device(x, "f32")
+    d = d0.clone()
+    o.optcc_allreduce_emulate(d, p, n, "f32", pl)
+    torch.cuda.synchronize()
+    fused = d.clone()
+    d.copy_(d0)
+    o.optcc_allreduce_emulate_slots(d, p, n, "f32", pl, 0, 2, 1)
+    torch.cuda.synchronize()
+    ref = oracle.run(oracle.Schedule(p, bw, n, k), "f32", x.copy(), 0, 2)
+    assert bits_equal(to_host(d, "f32"), ref)
+    o.optcc_allreduce_emulate_slots(d, p, n, "f32", pl, 2, 6, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(int_view(d), int_view(fused))
+    d.copy_(d0)
+    o.optcc_allreduce_emulate_slots(d, p, n, "f32", pl, 0, 6, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(int_view(d), int_view(fused))
+
+
 def test_work_stealing_threads_share_one_plan(o):
     """Four host threads, each on its own stream and buffers, run one
     work-stealing plan at once, three times each: concurrent launches take
