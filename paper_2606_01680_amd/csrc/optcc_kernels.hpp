@@ -357,7 +357,10 @@ __device__ void ring_lane(const KArgs &a, void *const *rp, const SegDesc &sd, co
 #pragma unroll
       for (int l = 0; l < L; ++l) v[l] = ld_in<D, W>(holder[l], e[l]);
     }
-    for (int t = 0; t + 1 < pp; ++t) {
+    // Every destination receives the same value, so the stores may go in
+    // any order: last hop first, so that the Stage-1 partials written most
+    // recently are overwritten while L2 still holds them.
+    for (int t = pp - 2; t >= 0; --t) {
 #pragma unroll
       for (int l = 0; l < L; ++l) st_fin<D, W>(rank(l, t), e[l], v[l]);
     }
@@ -718,18 +721,22 @@ __device__ __forceinline__ void server_lane(const KArgs &a, void *const *rp, con
     }
     have = true;
   }
+  // Slots 8 and 9 store one value everywhere, in any order: the servers
+  // last in the chain first (as in ring_lane), so that the partials their
+  // leaders and local GPUs wrote most recently are overwritten while L2
+  // still holds them.
   if (in_range(a, 8)) {  // slot 8: S4 allgather from the holder
 #pragma unroll
     for (int l = 0; l < L; ++l)
       if (!have) v[l] = ld_in<D, W, true>(hr(l, pp - 1, 0), e[l]);
-    for (int t = 0; t + 1 < pp; ++t) {
+    for (int t = pp - 2; t >= 0; --t) {
 #pragma unroll
       for (int l = 0; l < L; ++l) st_fin<D, W, true>(hr(l, t, 0), e[l], v[l]);
     }
     have = true;
   }
   if (in_range(a, 9)) {  // slot 9: N4 distribute on every healthy server
-    for (int t = 0; t < pp; ++t) {
+    for (int t = pp - 1; t >= 0; --t) {
       V gt[L];
 #pragma unroll
       for (int l = 0; l < L; ++l) gt[l] = have ? v[l] : ld_in<D, W, true>(hr(l, t, 0), e[l]);
@@ -768,7 +775,8 @@ __device__ __forceinline__ int section_of(const SegDesc &sd, int64_t u64) {
 
 // Every ring-section vector of one tile's lane, for a whole AllReduce
 // (slots [0, 6)), one GPU per server, one vector at a time: vector v's
-// Stage 1 chain carries, one per hop, the Stage 4 stores of vector v - 1,
+// Stage 1 chain carries, one per hop, the Stage 4 stores of vector v - 1
+// (last hop first, as in ring_lane),
 // and the stragglers' copies of vector v - 1 follow the chain, so that a
 // wave keeps loads in flight while it writes the previous vector's
 // allgather.  Each vector gets exactly the steps ring_lane gives it (other
@@ -818,7 +826,7 @@ __device__ void pipelined_ring_tile(const KArgs &a, void *const *rp, const SegDe
           v = add2<D, W>(buf[u], v);
           st_mid<D, W>(rank_at(j, 1 + t + u), e0, v);
           if (t + u + B < nh) buf[u] = ld_in<D, W>(rank_at(j, 1 + t + u + B), e0);
-          if (pend) st_fin<D, W>(rank_at(jp, t + u), ep, vp);
+          if (pend) st_fin<D, W>(rank_at(jp, nh - 1 - (t + u)), ep, vp);
         }
     }
     if (pend) {  // slot 5 of the previous vector
@@ -835,7 +843,7 @@ __device__ void pipelined_ring_tile(const KArgs &a, void *const *rp, const SegDe
     ep = e0;
   }
   if (pend) {
-    for (int t = 0; t + 1 < pp; ++t) st_fin<D, W>(rank_at(jp, t), ep, vp);
+    for (int t = pp - 2; t >= 0; --t) st_fin<D, W>(rank_at(jp, t), ep, vp);
     for (int i = 0; i < nside; ++i) st_fin<D, W>(a.ptr[pp + sfirst + i], ep, vp);
   }
 }
