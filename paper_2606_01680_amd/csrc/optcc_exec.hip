@@ -10,6 +10,7 @@
 #include <mutex>
 #include <string>
 #include <tuple>
+#include <utility>
 #include <vector>
 
 #include "optcc_internal.hpp"
@@ -187,21 +188,22 @@ int scratch_tables(const optcc_plan_t &pl, int tile_elems, hipStream_t stream, D
   return OPTCC_OK;
 }
 
-// Dynamic LDS that holds a launch to one workgroup per CU on the current
-// device (0 if the device cannot reserve that much), cached per device.
-// Measured on MI355X: chains of more than 32 healthy ranks run 2.6-8 %
+// Dynamic LDS (not used by the kernel) that holds a launch to at most n
+// workgroups per CU on the current device (0 if the device cannot reserve
+// that much), cached per device and n.  Measured on MI355X at one
+// workgroup per CU: chains of more than 32 healthy ranks run 2.6-8 %
 // faster at one workgroup (4 waves) per CU than at the 4 workgroups their
 // registers allow (P' = 39, 47, 62, 95, 124); shorter chains gain nothing
 // and p = 8 loses 10 %.  Server plans of more than 32 ranks (with per-XCD
 // tile runs): q16g4 -1.5 %, q32g4 -6 %, 8x8 and 16x8 GPUs -2 to -4 %,
 // 32x2 and 64x2 +1 to +4 %.
-int one_workgroup_per_cu_lds() {
+int workgroups_per_cu_lds(int n) {
   static std::mutex mu;
-  static std::map<int, int> cache;
+  static std::map<std::pair<int, int>, int> cache;
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (n < 1 || hipGetDevice(&dev) != hipSuccess) return 0;
   std::lock_guard<std::mutex> lk(mu);
-  auto it = cache.find(dev);
+  auto it = cache.find({dev, n});
   if (it != cache.end()) return it->second;
   int per_cu = 0, per_block = 0;
   int v = 0;
@@ -209,11 +211,14 @@ int one_workgroup_per_cu_lds() {
           hipSuccess &&
       hipDeviceGetAttribute(&per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
           hipSuccess) {
+    // fixed + want is just over 1/(n+1) of the CU's LDS, so n + 1
+    // workgroups never fit, and n still do (n * 256 bytes of margin is far
+    // below per_cu / (n + 1) for the n used here)
     const int fixed = (int)(sizeof(void *) * kMaxRanks);  // the kernel's rank-pointer table
-    const int want = per_cu / 2 + 256 - fixed;           // fixed + want > half of the CU's LDS
-    if (want > 0 && fixed + want <= per_block) v = want;
+    const int want = per_cu / (n + 1) + 256 - fixed;
+    if (want > 0 && fixed + want <= per_block && (int64_t)n * (fixed + want) <= per_cu) v = want;
   }
-  cache[dev] = v;
+  cache[{dev, n}] = v;
   return v;
 }
 
@@ -363,7 +368,20 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
     for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   }
-  a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? one_workgroup_per_cu_lds() : 0;
+  a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? workgroups_per_cu_lds(1) : 0;
+  // The mid-size short chains of 6 or 7 healthy ranks with at least
+  // kThreePerCuMinBytes of 16-byte-aligned rank buffers run at three
+  // workgroups per CU instead of the four their registers allow: with fewer
+  // lanes in flight more Stage-1 partial sums are still in L2 when Stage 4
+  // overwrites them.  Measured (back-to-back calls, results bit for bit
+  // equal): p = 8 with one straggler at 0.875, fp32, from 480 MiB to
+  // 1.75 GiB of rank buffers 1.5-5 % faster (768 MiB equal), int32 1.7-2.9 %,
+  // the straggler at 0.5 or 0.25 2.2-4.8 %, p = 9 with two stragglers
+  // 1.4-2.2 %, p = 7 0-2.7 %; p = 8 at 384 and 448 MiB 2 and 1.3 % slower;
+  // chains of 3-5 healthy ranks gain or lose up to 3 % with the size, and
+  // element-aligned buffers lose 30-50 %, so neither takes it.
+  if (mid_short && vec16 && pl->pp >= kThreePerCuMinHealthy && buf_bytes >= kThreePerCuMinBytes)
+    a.occ_lds = workgroups_per_cu_lds(3);
   // The same mid-size short chains take each vector's Stage 4 stores into
   // the next vector's Stage 1 chain (the kernel's pipelined ring tiles).
   // Measured against one vector at a time (back-to-back calls, every result

@@ -68,6 +68,10 @@ constexpr int64_t kXcdRunsMaxTiles = 2048;
 constexpr int kOneVectorMaxHealthy = 7;
 constexpr int64_t kOneVectorMinBytes = (int64_t)16 << 20;
 constexpr int64_t kOneVectorMaxBytes = (int64_t)2 << 30;
+// of those, chains of at least this many healthy ranks with at least this
+// many bytes of 16-byte-aligned rank buffers run three workgroups per CU
+constexpr int kThreePerCuMinHealthy = 6;
+constexpr int64_t kThreePerCuMinBytes = (int64_t)512 << 20;
 
 struct KArgs {
   const TileDesc *tiles;

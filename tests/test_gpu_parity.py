@@ -867,6 +867,38 @@ def test_random_plans_at_rule_sizes(o):
         torch.cuda.empty_cache()
 
 
+THREE_PER_CU_CASES = [
+    # 6-7 healthy ranks at the 512 MiB edge of the three-workgroups-per-CU
+    # launch: just above (three per CU), just below (four per CU), and
+    # element-aligned buffers above it (four per CU, one element per access)
+    ("p=8 at 0.875, fp32, 512 MiB", 8, {7: 0.875}, 1 << 24, "f32"),
+    ("p=8 at 0.875, fp32, 512 MiB - 128 B", 8, {7: 0.875}, (1 << 24) - 4, "f32"),
+    ("p=7 at 0.5, int32, 512 MiB + 80 B", 7, {6: 0.5}, 19173964, "i32"),
+    ("p=9, two stragglers, fp32, odd N", 9, {7: 0.5, 8: 0.5}, (1 << 24) + 1, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", THREE_PER_CU_CASES, ids=[c[0] for c in THREE_PER_CU_CASES])
+def test_three_workgroups_per_cu_edge(o, case):
+    """Short chains around the buffer size from which the launch holds three
+    workgroups per CU: every element of every rank bit for bit against the
+    oracle's full serial run."""
+    label, p, strag, n, dtype = case
+    _say(f"case three-per-CU edge: {label}: p={p} n={n} dtype={dtype}")
+    bw = _bw(p, strag)
+    pl = o.optcc_plan(p, bw, n, 64)
+    x = rand_inputs(dtype, p, n, 4242 + p)
+    d = to_device(x, dtype)
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    got = to_host(d, dtype)
+    del d
+    ref = oracle.run(oracle.Schedule(p, bw, n, 64), dtype, x)
+    assert bits_equal(got, ref), label
+    del x, got, ref
+    torch.cuda.empty_cache()
+
+
 def test_one_graph_of_several_allreduces(o):
     """Several AllReduces with different plans and element types (bubble
     filling, several stragglers, a 40-rank chain launched at one workgroup
