@@ -382,6 +382,16 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // element-aligned buffers lose 30-50 %, so neither takes it.
   if (mid_short && vec16 && pl->pp >= kThreePerCuMinHealthy && buf_bytes >= kThreePerCuMinBytes)
     a.occ_lds = workgroups_per_cu_lds(3);
+  // bf16 chains of kBf16ThreePerCuMinHealthy to kTwoVectorMaxHealthy
+  // healthy ranks (one GPU per server, 16-byte path) run at three
+  // workgroups per CU as well.  Measured (same method): p16_bf16 at 2^20 /
+  // 2^22 / 2^24 / 2^26 elements per rank 1.6 / 1.7 / 0.7 / 1.1 % faster,
+  // p = 24 at 2^22 and 2^24 3.7 and 1.4 %, p = 33 1.4 %, p = 18 with two
+  // stragglers 1.0 %; p = 20 at 2^20 1.4 % slower; shorter chains equal or
+  // slower (p = 12 0 %, p = 10 up to 4 %, p = 9 0.7 %).
+  if (!servers && dtype == OPTCC_BF16 && vec16 && pl->pp >= kBf16ThreePerCuMinHealthy &&
+      pl->pp <= kTwoVectorMaxHealthy)
+    a.occ_lds = workgroups_per_cu_lds(3);
   // The same mid-size short chains take each vector's Stage 4 stores into
   // the next vector's Stage 1 chain (the kernel's pipelined ring tiles).
   // Measured against one vector at a time (back-to-back calls, every result

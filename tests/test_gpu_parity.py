@@ -875,14 +875,21 @@ THREE_PER_CU_CASES = [
     ("p=8 at 0.875, fp32, 512 MiB - 128 B", 8, {7: 0.875}, (1 << 24) - 4, "f32"),
     ("p=7 at 0.5, int32, 512 MiB + 80 B", 7, {6: 0.5}, 19173964, "i32"),
     ("p=9, two stragglers, fp32, odd N", 9, {7: 0.5, 8: 0.5}, (1 << 24) + 1, "f32"),
+    # bf16 chains of 13-32 healthy ranks (three per CU at any size) and
+    # just outside that range
+    ("p=14 at 0.5, bf16, 13 healthy", 14, {13: 0.5}, 3 << 20, "bf16"),
+    ("p=13 at 0.5, bf16, 12 healthy", 13, {12: 0.5}, 3 << 20, "bf16"),
+    ("p=33 at 0.75, bf16, 32 healthy", 33, {0: 0.75}, (1 << 20) + 8, "bf16"),
+    ("p=16 at 0.5, bf16, odd N", 16, {15: 0.5}, (1 << 21) + 3, "bf16"),
 ]
 
 
 @pytest.mark.parametrize("case", THREE_PER_CU_CASES, ids=[c[0] for c in THREE_PER_CU_CASES])
-def test_three_workgroups_per_cu_edge(o, case):
-    """Short chains around the buffer size from which the launch holds three
-    workgroups per CU: every element of every rank bit for bit against the
-    oracle's full serial run."""
+def test_three_workgroups_per_cu_edges(o, case):
+    """Plans on both sides of the launch rules that hold three workgroups per
+    CU (short fp32/int32 chains from 512 MiB of rank buffers, bf16 chains of
+    13-32 healthy ranks): every element of every rank bit for bit against
+    the oracle's full serial run."""
     label, p, strag, n, dtype = case
     _say(f"case three-per-CU edge: {label}: p={p} n={n} dtype={dtype}")
     bw = _bw(p, strag)
