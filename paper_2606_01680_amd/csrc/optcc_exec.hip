@@ -344,6 +344,18 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   const bool mid_short = !servers && es == 4 && pl->pp >= 3 && pl->pp <= kOneVectorMaxHealthy &&
                          buf_bytes >= kOneVectorMinBytes && buf_bytes < kOneVectorMaxBytes;
   if (mid_short && pl->pp >= 5) tile_elems = std::min(tile_elems, vec_tile);
+  // Longer one-GPU-per-server chains take one vector per lane per tile too
+  // (1024 elements for 32-bit types; 2-byte types have it already), so a
+  // workgroup moves on to a new tile after every chain.  Measured against
+  // 2048-element tiles (back-to-back calls, results bit for bit equal; the
+  // tile count also decides per-XCD runs against work stealing below):
+  // p64_f32 at 2^24 elements per rank 3.0 % faster, at 2^23 2.7 %, 2^22
+  // equal; p128_f32 at 2^21 / 2^22 1.8 / 5.3 %, 2^23-2^25 0-0.6 %; one or
+  // two stragglers with 33-256 ranks, fp32 and int32, 2^21-2^25: 0.5-14 %
+  // faster in 27 of 30 plans, equal in one, 0.3 and 2.3 % slower in two
+  // (48 ranks at 2^22).  Server plans were mixed (q32g4_f32 1.2 % slower,
+  // q16g4_f32 0.4-3 % faster) and keep their tiles.
+  if (long_chain && !servers) tile_elems = std::min(tile_elems, vec_tile);
   const int64_t ntiles = tile_count(*pl, tile_elems);
   if (noalloc && scratch_bytes(*pl, ntiles) > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
     return fail(OPTCC_EUNSUPPORTED,

@@ -616,12 +616,13 @@ def test_threads_share_one_plan(o):
         assert bits_equal(to_host(devs[dt], dt), ref), dt
 
 
-# Long chains (more than 32 healthy ranks, one workgroup per CU) whose
-# tiles outnumber the per-XCD-run limit (2,048) run as a persistent grid
-# that takes tiles from a device counter (work stealing); bf16 keeps the
-# static order.  Sizes just above the limit, ragged.
+# Long chains (more than 32 healthy ranks, one workgroup per CU, tiles of
+# one vector per lane) whose tiles outnumber the per-XCD-run limit (2,048)
+# run as a persistent grid that takes tiles from a device counter (work
+# stealing); bf16 keeps the static order.  Sizes above the limit, ragged,
+# one just above it.
 STEAL = [(40, {5: 0.6}, 2048 * 2100 + 77, 8), (70, {3: 0.875}, 2048 * 2200 + 130, 16),
-         (36, {}, 2048 * 2300 + 3, 4)]
+         (36, {}, 2048 * 2300 + 3, 4), (100, {7: 0.5, 60: 0.75}, 1024 * 2049 + 5, 8)]
 
 
 @pytest.mark.parametrize("p,slow,n,k", STEAL)
