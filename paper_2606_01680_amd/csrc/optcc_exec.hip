@@ -316,10 +316,11 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // Per-XCD tile runs: for short chains, for every server plan (beyond 32
   // ranks, together with one workgroup per CU, 2.4-27 % faster than with
   // neither) and for longer one-GPU-per-server chains whose tiles are more
-  // than one round of resident workgroups and at most kXcdRunsMaxTiles (p = 64
-  // and 128 at 2^19-2^22 elements per rank: 2.4-14 % faster; at 4096 tiles
-  // -8 % at p = 64, +4 % at p = 128; from 8192 tiles 0.8-0.9 % slower; with
-  // one round of tiles, 2^17-2^18 elements per rank, 3-5 % slower).
+  // than one round of resident workgroups and at most kXcdRunsMaxTiles
+  // (measured with 2048-element tiles, p = 64 and 128 at 2^19-2^22 elements
+  // per rank: 2.4-14 % faster; at 4096 tiles -8 % at p = 64, +4 % at
+  // p = 128; from 8192 tiles 0.8-0.9 % slower; with one round of tiles,
+  // 2^17-2^18 elements per rank, 3-5 % slower).
   // bf16 with one GPU per server keeps full occupancy: eight elements per
   // 16-byte vector, each widened by a shift, added in fp32 and rounded back,
   // gain from the latency hiding of several waves (one workgroup per CU:
