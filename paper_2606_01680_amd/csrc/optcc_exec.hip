@@ -413,13 +413,22 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // lose 1-8 % (p = 64, 128), so they keep one vector at a time.
   a.pipe = mid_short ? 1 : 0;
   bool runs = servers || two;
-  if (long_chain && !servers && ntiles <= kXcdRunsMaxTiles) {
+  // With one-vector tiles, chains of fewer than kXcdRunsWideHealthy healthy
+  // ranks keep the per-XCD runs up to kXcdRunsMaxTilesMid tiles.  Measured
+  // at 4096 tiles against work stealing (back-to-back calls, results bit
+  // for bit equal): p64_f32 at 2^22 elements per rank 2.7 % faster, 48
+  // ranks 1.5 %, 48 ranks int32 with two stragglers 3.8 %, 80 ranks int32
+  // 0.5 %; 96 and 128 ranks 2.4 and 3.5 % slower; at 8192 tiles runs were
+  // slower for every chain (36 ranks 1.5 %, p64 2.3 %, 48 ranks 3.6 %,
+  // p128 11 %).
+  const int64_t runs_max = pl->pp < kXcdRunsWideHealthy ? kXcdRunsMaxTilesMid : kXcdRunsMaxTiles;
+  if (long_chain && !servers && ntiles <= runs_max) {
     const int resident = resident_workgroups(a, dtype, servers, vec16, two_vec);
     runs = resident <= 0 || ntiles > resident;
   }
   a.xcd_runs = runs ? 1 : 0;
   // Work stealing for the same long chains at one workgroup per CU when
-  // their tiles take the identity order (more than kXcdRunsMaxTiles): a
+  // their tiles take the identity order (more than runs_max): a
   // grid of the resident workgroups takes tiles from a device counter.  The
   // eight XCDs do not run equally fast (per-wave timestamps of p128_f32:
   // XCDs 1, 3, 5, 7 spend about 5 % longer per tile than 0, 2, 4, 6), and

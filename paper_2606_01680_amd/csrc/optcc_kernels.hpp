@@ -59,8 +59,12 @@ constexpr bool kNtMid = OPTCC_NT_MID;
 // vectors per lane in lockstep (measured faster for short chains)
 constexpr int kTwoVectorMaxHealthy = 32;
 // longer one-GPU-per-server chains take per-XCD tile runs up to this many
-// tiles (measured faster at 2048 tiles and below, slower from 8192)
+// tiles (measured faster at 2048 tiles and below, slower from 8192), and
+// up to kXcdRunsMaxTilesMid when they have fewer than kXcdRunsWideHealthy
+// healthy ranks (faster with runs at 4096 tiles too)
 constexpr int64_t kXcdRunsMaxTiles = 2048;
+constexpr int64_t kXcdRunsMaxTilesMid = 4096;
+constexpr int kXcdRunsWideHealthy = 90;
 // mid-size messages on one-GPU-per-server chains of 32-bit elements with at
 // most this many healthy ranks, whose rank buffers total at least
 // kOneVectorMinBytes and less than kOneVectorMaxBytes, run one vector per

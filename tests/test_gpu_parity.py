@@ -113,7 +113,9 @@ def test_mid_size_short_chains_bit_exact(o, dtype, p, slow, n, k):
     assert bits_equal(got, ref)
 
 
-@pytest.mark.parametrize("p,n", [(40, 1 << 17), (64, 1 << 18), (64, (1 << 19) + 4097)])
+@pytest.mark.parametrize("p,n", [(40, 1 << 17), (64, 1 << 18), (64, (1 << 19) + 4097),
+                                 # 62 healthy ranks keep the runs up to 4,096 tiles
+                                 (64, 1024 * 4000 + 3)])
 def test_long_chains_one_round_of_tiles(o, p, n):
     """Long chains whose tiles fit in one round of resident workgroups take
     the identity tile order, more tiles the per-XCD runs: both bit for bit."""
@@ -617,12 +619,13 @@ def test_threads_share_one_plan(o):
 
 
 # Long chains (more than 32 healthy ranks, one workgroup per CU, tiles of
-# one vector per lane) whose tiles outnumber the per-XCD-run limit (2,048)
-# run as a persistent grid that takes tiles from a device counter (work
-# stealing); bf16 keeps the static order.  Sizes above the limit, ragged,
-# one just above it.
+# one vector per lane) whose tiles outnumber the per-XCD-run limit (2,048;
+# 4,096 below 90 healthy ranks) run as a persistent grid that takes tiles
+# from a device counter (work stealing); bf16 keeps the static order.
+# Sizes above the limit, ragged, two just above it.
 STEAL = [(40, {5: 0.6}, 2048 * 2100 + 77, 8), (70, {3: 0.875}, 2048 * 2200 + 130, 16),
-         (36, {}, 2048 * 2300 + 3, 4), (100, {7: 0.5, 60: 0.75}, 1024 * 2049 + 5, 8)]
+         (36, {}, 2048 * 2300 + 3, 4), (100, {7: 0.5, 60: 0.75}, 1024 * 2049 + 5, 8),
+         (64, {63: 0.5, 62: 0.75}, 1024 * 4100 + 5, 16)]
 
 
 @pytest.mark.parametrize("p,slow,n,k", STEAL)
