@@ -418,9 +418,10 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // at 4096 tiles against work stealing (back-to-back calls, results bit
   // for bit equal): p64_f32 at 2^22 elements per rank 2.7 % faster, 48
   // ranks 1.5 %, 48 ranks int32 with two stragglers 3.8 %, 80 ranks int32
-  // 0.5 %; 96 and 128 ranks 2.4 and 3.5 % slower; at 8192 tiles runs were
-  // slower for every chain (36 ranks 1.5 %, p64 2.3 %, 48 ranks 3.6 %,
-  // p128 11 %).
+  // 0.5 %, 64 ranks bf16 (no stealing: against the identity order) 0.3 %;
+  // 96 and 128 ranks 2.4 and 3.5 % slower (bf16: 5 %); at 8192 tiles runs
+  // were slower for every chain (36 ranks 1.5 %, p64 2.3 %, 48 ranks
+  // 3.6 %, p128 11 %, bf16 2.4-4 %).
   const int64_t runs_max = pl->pp < kXcdRunsWideHealthy ? kXcdRunsMaxTilesMid : kXcdRunsMaxTiles;
   if (long_chain && !servers && ntiles <= runs_max) {
     const int resident = resident_workgroups(a, dtype, servers, vec16, two_vec);
