@@ -910,6 +910,37 @@ def test_three_workgroups_per_cu_edges(o, case):
     torch.cuda.empty_cache()
 
 
+def test_random_large_short_chains(o):
+    """Four seeded random plans of 6-8 healthy ranks with 480 MiB to 1.9 GiB
+    of rank buffers (the range where 6-7 healthy ranks launch at three
+    workgroups per CU and 8 take two vectors per lane), fp32 and int32, one
+    or two stragglers: every element of every rank bit for bit against the
+    oracle's full serial run."""
+    rng = np.random.default_rng(2606)
+    for i in range(4):
+        p = int(rng.integers(7, 10))
+        m = 1 if p < 9 else int(rng.integers(1, 3))
+        bw = [1.0] * p
+        for r in rng.choice(p, size=m, replace=False):
+            bw[int(r)] = float(rng.integers(1, 8)) / 8
+        dtype = ("f32", "i32")[i % 2]
+        lo, hi = (480 << 20) // (4 * p), (1900 << 20) // (4 * p)
+        n = int(rng.integers(lo, hi)) // 4 * 4 + int(rng.integers(0, 4))
+        k = 4 * int(rng.integers(4, 33))
+        _say(f"case large short chain #{i}: p={p} n={n} k={k} dtype={dtype} bw={sorted(set(bw))}")
+        pl = o.optcc_plan(p, bw, n, k)
+        x = rand_inputs(dtype, p, n, 9100 + i)
+        d = to_device(x, dtype)
+        o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+        torch.cuda.synchronize()
+        got = to_host(d, dtype)
+        del d
+        ref = oracle.run(oracle.Schedule(p, bw, n, k), dtype, x)
+        assert bits_equal(got, ref), i
+        del x, got, ref
+        torch.cuda.empty_cache()
+
+
 def test_one_graph_of_several_allreduces(o):
     """Several AllReduces with different plans and element types (bubble
     filling, several stragglers, a 40-rank chain launched at one workgroup
