@@ -76,6 +76,11 @@ constexpr int64_t kOneVectorMaxBytes = (int64_t)2 << 30;
 // many bytes of 16-byte-aligned rank buffers run three workgroups per CU
 constexpr int kThreePerCuMinHealthy = 6;
 constexpr int64_t kThreePerCuMinBytes = (int64_t)512 << 20;
+// 32-bit chains of at least this many (and at most kTwoVectorMaxHealthy)
+// healthy ranks with at least this many bytes of 16-byte-aligned rank
+// buffers run one workgroup per CU (two vectors per lane)
+constexpr int kTwoVecOnePerCuMinHealthy = 11;
+constexpr int64_t kTwoVecOnePerCuMinBytes = (int64_t)1 << 30;
 // bf16 chains of at least this many (and at most kTwoVectorMaxHealthy)
 // healthy ranks, 16-byte-aligned, run three workgroups per CU at any size
 constexpr int kBf16ThreePerCuMinHealthy = 13;

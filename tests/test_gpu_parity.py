@@ -885,15 +885,23 @@ THREE_PER_CU_CASES = [
     ("p=13 at 0.5, bf16, 12 healthy", 13, {12: 0.5}, 3 << 20, "bf16"),
     ("p=33 at 0.75, bf16, 32 healthy", 33, {0: 0.75}, (1 << 20) + 8, "bf16"),
     ("p=16 at 0.5, bf16, odd N", 16, {15: 0.5}, (1 << 21) + 3, "bf16"),
+    # fp32/int32 chains of 11-32 healthy ranks from 1 GiB of buffers run one
+    # workgroup per CU; 10 healthy ranks and smaller buffers keep two
+    ("p=12 at 0.5, fp32, 11 healthy, 1 GiB", 12, {11: 0.5}, 22369624, "f32"),
+    ("p=11 at 0.5, int32, 10 healthy, 1 GiB", 11, {10: 0.5}, 24403352, "i32"),
+    ("p=16 at 0.875, fp32, 1 GiB - 256 B", 16, {15: 0.875}, (1 << 24) - 4, "f32"),
+    ("p=33 at 0.5, int32, 32 healthy, 1 GiB + 7 KiB", 33, {32: 0.5}, 8134464, "i32"),
+    ("p=16 at 0.5, fp32, odd N, 1 GiB + 64 B", 16, {15: 0.5}, (1 << 24) + 1, "f32"),
 ]
 
 
 @pytest.mark.parametrize("case", THREE_PER_CU_CASES, ids=[c[0] for c in THREE_PER_CU_CASES])
 def test_three_workgroups_per_cu_edges(o, case):
-    """Plans on both sides of the launch rules that hold three workgroups per
-    CU (short fp32/int32 chains from 512 MiB of rank buffers, bf16 chains of
-    13-32 healthy ranks): every element of every rank bit for bit against
-    the oracle's full serial run."""
+    """Plans on both sides of the launch rules that change the workgroups
+    per CU (three: short fp32/int32 chains from 512 MiB of rank buffers and
+    bf16 chains of 13-32 healthy ranks; one: fp32/int32 chains of 11-32
+    healthy ranks from 1 GiB): every element of every rank bit for bit
+    against the oracle's full serial run."""
     label, p, strag, n, dtype = case
     _say(f"case three-per-CU edge: {label}: p={p} n={n} dtype={dtype}")
     bw = _bw(p, strag)
