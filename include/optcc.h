@@ -157,7 +157,7 @@ void optcc_plan_free(optcc_plan_t *plan);
  * its tables).  These checks are made before any device call.
  *
  * Launch order of the tiles (never the result): plans of more than 32
- * healthy ranks whose elements are not bf16 and whose tiles outnumber 2,048
+ * healthy ranks with one GPU per server whose tiles outnumber 2,048
  * (4,096 with fewer than 90 healthy ranks; a tile is one 16-byte vector per
  * lane, 1,024 elements for 32-bit types, for these plans)
  * run a grid of the resident workgroups that take tiles from a device

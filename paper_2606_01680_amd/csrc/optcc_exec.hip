@@ -321,11 +321,13 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // per rank: 2.4-14 % faster; at 4096 tiles -8 % at p = 64, +4 % at
   // p = 128; from 8192 tiles 0.8-0.9 % slower; with one round of tiles,
   // 2^17-2^18 elements per rank, 3-5 % slower).
-  // bf16 with one GPU per server keeps full occupancy: eight elements per
-  // 16-byte vector, each widened by a shift, added in fp32 and rounded back,
-  // gain from the latency hiding of several waves (one workgroup per CU:
-  // p = 64 +0.5 %, p = 128 +1.5 %); bf16 server plans of more than 32 ranks
-  // gain from it (16 x 4 -3 %, 8 x 8 -1.3 %), like fp16, int32 and fp32.
+  // bf16 long chains run one workgroup per CU as well (and take work
+  // stealing like the others).  Measured against full occupancy (back-to-
+  // back calls, results bit for bit equal): 34-256 ranks, 2^21-2^25
+  // elements per rank, 2.9-16 % faster (p = 128 at 2^23 985 -> 891 us,
+  // 256 ranks at 2^21 584 -> 504 us); p = 128 at 2^20 1 % and 64 ranks
+  // with bubble filling at 2^23 0.5 % slower.  bf16 server plans of more
+  // than 32 ranks gain from it too (16 x 4 -3 %, 8 x 8 -1.3 %).
   // A single-hop chain (two healthy ranks, p = 3 with one straggler) runs
   // one vector per lane in the identity order: 8 % faster than two vectors
   // with XCD runs (p = 4 is fastest with both).
@@ -381,7 +383,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     for (int i = 0; i < pl->pp; ++i) a.ptr[i] = bufs[pl->ring[(size_t)i]];
     for (int i = 0; i < pl->m; ++i) a.ptr[pl->pp + i] = bufs[pl->strag[(size_t)i]];
   }
-  a.occ_lds = long_chain && (dtype != OPTCC_BF16 || servers) ? workgroups_per_cu_lds(1) : 0;
+  a.occ_lds = long_chain ? workgroups_per_cu_lds(1) : 0;
   // 32-bit chains of 11-32 healthy ranks (one GPU per server, two vectors
   // per lane, 178 VGPRs: two workgroups per CU) with at least
   // kTwoVecOnePerCuMinBytes of 16-byte-aligned rank buffers run one
@@ -450,9 +452,9 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // Measured (back-to-back calls, results bit for bit equal): p = 128 fp32
   // at 2^23 / 2^24 / 2^25 elements per rank 2.1 / 4.2 / 3.6 % faster, p = 64
   // 3.4 / 2.2 / 2.5 %, int32 p = 128 at 2^24 2.6 %, one straggler at 0.875
-  // with p = 96 (P2P chunks) 2.9 %, p = 40 and 48 1.5-3.2 %; bf16 (full
-  // occupancy) 7.6 % slower, and with per-XCD runs (fewer tiles) it gains
-  // nothing, so neither takes it.  Not under graph capture: a captured
+  // with p = 96 (P2P chunks) 2.9 %, p = 40 and 48 1.5-3.2 %; bf16 long
+  // chains at one workgroup per CU likewise (with the gain of that
+  // occupancy, above).  Not under graph capture: a captured
   // launch keeps its counter block, and replays of the graph on two streams
   // at once would share it; the no-allocation entry point keeps the static
   // order too.

@@ -621,22 +621,25 @@ def test_threads_share_one_plan(o):
 # Long chains (more than 32 healthy ranks, one workgroup per CU, tiles of
 # one vector per lane) whose tiles outnumber the per-XCD-run limit (2,048;
 # 4,096 below 90 healthy ranks) run as a persistent grid that takes tiles
-# from a device counter (work stealing); bf16 keeps the static order.
-# Sizes above the limit, ragged, two just above it.
+# from a device counter (work stealing), every element type.  Sizes above
+# the limit, ragged, two just above it.
 STEAL = [(40, {5: 0.6}, 2048 * 2100 + 77, 8), (70, {3: 0.875}, 2048 * 2200 + 130, 16),
          (36, {}, 2048 * 2300 + 3, 4), (100, {7: 0.5, 60: 0.75}, 1024 * 2049 + 5, 8),
-         (64, {63: 0.5, 62: 0.75}, 1024 * 4100 + 5, 16)]
+         (64, {63: 0.5, 62: 0.75}, 1024 * 4100 + 5, 16),
+         # 98 healthy ranks, 2,101 tiles of 2048 2-byte elements: bf16 and fp16 steal too
+         (100, {7: 0.5, 60: 0.75}, 2048 * 2100 + 9, 8)]
 
 
 @pytest.mark.parametrize("p,slow,n,k", STEAL)
 def test_work_stealing_launches(o, p, slow, n, k):
     """Three calls in a row of a work-stealing plan (the counters reset
-    themselves at the end of each launch), fp32, int32 and fp16: the first
-    result equals the oracle on every element, the others equal the first."""
+    themselves at the end of each launch), fp32, int32, fp16 and bf16: the
+    first result equals the oracle on every element, the others equal the
+    first."""
     bw = _bw(p, slow)
     pl = o.optcc_plan(p, bw, n, k)
     sched = oracle.Schedule(p, bw, n, k)
-    for dtype in ("f32", "i32", "f16"):
+    for dtype in ("f32", "i32", "f16", "bf16"):
         _say(f"case work stealing p={p} n={n} k={k} dtype={dtype}")
         x = rand_inputs(dtype, p, n, 90 + p)
         d = to_device(x, dtype)
