@@ -385,16 +385,19 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   }
   a.occ_lds = long_chain ? workgroups_per_cu_lds(1) : 0;
   // 32-bit chains of 11-32 healthy ranks (one GPU per server, two vectors
-  // per lane, 178 VGPRs: two workgroups per CU) with at least
-  // kTwoVecOnePerCuMinBytes of 16-byte-aligned rank buffers run one
-  // workgroup per CU too.  Measured (back-to-back calls, results bit for bit
-  // equal), from 1 GiB of buffers: 12-16 ranks 1.3-4.9 % faster, 20-33
-  // ranks 2.0-3.2 %, with bubble filling 1.8 %, two stragglers -0.2 to
-  // +1.2 %, int32 like fp32; 10 and 11 ranks 1-2 % slower, p = 8 9 %.
-  // Below 1 GiB the effect swings both ways (256 MiB at 32 ranks +7 %,
-  // 384 MiB at 12 ranks int32 -15 %, 64 MiB at 16 ranks -14.5 %).  Server
-  // plans of 16 ranks split (4 x 4 +3.5 %, 8 x 2 -4.4 %) and are left out.
-  if (two_vec && vec16 && !servers && pl->pp >= kTwoVecOnePerCuMinHealthy &&
+  // per lane, 178 VGPRs: two workgroups per CU) with at most one straggler
+  // and at least kTwoVecOnePerCuMinBytes of 16-byte-aligned rank buffers
+  // run one workgroup per CU too.  Measured (back-to-back calls, results
+  // bit for bit equal), from 1 GiB of buffers: one straggler, 12-16 ranks
+  // 1.3-4.9 % faster, 20-33 ranks 2.0-3.2 %, with bubble filling 1.8 %,
+  // int32 like fp32; rings of 12-32 ranks 2.3-6.5 %; 10 and 11 ranks 1-2 %
+  // slower, p = 8 9 %.  Several stragglers split with the chain length
+  // (13-14 healthy ranks 0.5-4.6 % slower, 18-29 from 1 % slower to 2.3 %
+  // faster) and keep two per CU.  Below 1 GiB the effect swings both ways
+  // (256 MiB at 32 ranks +7 %, 384 MiB at 12 ranks int32 -15 %, 64 MiB at
+  // 16 ranks -14.5 %).  Server plans of 16 ranks split (4 x 4 +3.5 %,
+  // 8 x 2 -4.4 %) and are left out.
+  if (two_vec && vec16 && !servers && pl->m <= 1 && pl->pp >= kTwoVecOnePerCuMinHealthy &&
       buf_bytes >= kTwoVecOnePerCuMinBytes)
     a.occ_lds = workgroups_per_cu_lds(1);
   // The mid-size short chains of 6 or 7 healthy ranks with at least

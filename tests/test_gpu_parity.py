@@ -895,6 +895,9 @@ THREE_PER_CU_CASES = [
     ("p=16 at 0.875, fp32, 1 GiB - 256 B", 16, {15: 0.875}, (1 << 24) - 4, "f32"),
     ("p=33 at 0.5, int32, 32 healthy, 1 GiB + 7 KiB", 33, {32: 0.5}, 8134464, "i32"),
     ("p=16 at 0.5, fp32, odd N, 1 GiB + 64 B", 16, {15: 0.5}, (1 << 24) + 1, "f32"),
+    ("p=16, three stragglers, fp32, 1 GiB (two per CU)", 16, {0: 0.5, 1: 0.75, 15: 0.875},
+     1 << 24, "f32"),
+    ("p=16 ring, int32, 1 GiB", 16, {}, 1 << 24, "i32"),
 ]
 
 
