@@ -395,10 +395,14 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // (13-14 healthy ranks 0.5-4.6 % slower, 18-29 from 1 % slower to 2.3 %
   // faster) and keep two per CU.  Below 1 GiB the effect swings both ways
   // (256 MiB at 32 ranks +7 %, 384 MiB at 12 ranks int32 -15 %, 64 MiB at
-  // 16 ranks -14.5 %).  Server plans of 16 ranks split (4 x 4 +3.5 %,
-  // 8 x 2 -4.4 %) and are left out.
-  if (two_vec && vec16 && !servers && pl->m <= 1 && pl->pp >= kTwoVecOnePerCuMinHealthy &&
-      buf_bytes >= kTwoVecOnePerCuMinBytes)
+  // 16 ranks -14.5 %).  Server plans of at most 32 ranks (two vectors
+  // per lane as well) take it with 4 or more GPUs per server: 4 x 4,
+  // 5 x 4 (int32), 6 x 4 and 8 x 4 servers 2.7-4.0 % faster, 3 x 8 and
+  // 4 x 8 0.3-0.4 %; with 2 GPUs per server it splits (16 x 2 +1.4 %,
+  // 12 x 2 -0.7 %, 8 x 2 -3.4 %).
+  const bool two_vec_one_per_cu =
+      servers ? pl->g >= 4 : (pl->m <= 1 && pl->pp >= kTwoVecOnePerCuMinHealthy);
+  if (two_vec && vec16 && two_vec_one_per_cu && buf_bytes >= kTwoVecOnePerCuMinBytes)
     a.occ_lds = workgroups_per_cu_lds(1);
   // The mid-size short chains of 6 or 7 healthy ranks with at least
   // kThreePerCuMinBytes of 16-byte-aligned rank buffers run at three

@@ -180,6 +180,23 @@ def test_server_tile_lengths_bit_exact(o, dtype, q, g, slow, n, k):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("dtype,q,g,slow,n", [
+    # at most 32 ranks, 32-bit elements, from 1 GiB of buffers: one
+    # workgroup per CU with 4 or more GPUs per server, two with 2
+    ("f32", 4, 4, {3: 0.5}, (1 << 24) + 4),
+    ("i32", 8, 2, {0: 0.5}, (1 << 24) + 8),
+    ("f32", 4, 4, {1: 0.875}, (1 << 24) - 4),
+])
+def test_server_occupancy_edges(o, dtype, q, g, slow, n):
+    """Server plans around the 1 GiB edge of the one-workgroup-per-CU
+    launch, bit for bit against the oracle on every element."""
+    from gpu_util import bits_equal
+    _say(f"case servers occupancy dtype={dtype} q={q} g={g} slow={slow} n={n}")
+    x, ref, got = _run_both(o, q, g, slow, n, 24, dtype, seed=q * 7 + g)
+    assert bits_equal(got, ref)
+
+
+@pytest.mark.gpu
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "i32", "f16"])
 @pytest.mark.parametrize("q,g,slow", [(3, 2, {2: 0.5}), (4, 3, {1: 0.875}), (5, 4, {0: 0.5})])
 @pytest.mark.parametrize("launches", [1, 0])
