@@ -356,8 +356,9 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // equal; p128_f32 at 2^21 / 2^22 1.8 / 5.3 %, 2^23-2^25 0-0.6 %; one or
   // two stragglers with 33-256 ranks, fp32 and int32, 2^21-2^25: 0.5-14 %
   // faster in 27 of 30 plans, equal in one, 0.3 and 2.3 % slower in two
-  // (48 ranks at 2^22).  Server plans were mixed (q32g4_f32 1.2 % slower,
-  // q16g4_f32 0.4-3 % faster) and keep their tiles.
+  // (48 ranks at 2^22; both faster again with the 4,096-tile runs limit
+  // below).  Server plans were mixed (q32g4_f32 1.2 % slower, q16g4_f32
+  // 0.4-3 % faster) and keep their tiles.
   if (long_chain && !servers) tile_elems = std::min(tile_elems, vec_tile);
   const int64_t ntiles = tile_count(*pl, tile_elems);
   if (noalloc && scratch_bytes(*pl, ntiles) > (size_t)OPTCC_NOALLOC_SCRATCH_BYTES)
