@@ -435,6 +435,15 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // 3 / 1.2 / 1.5 % faster, int32 at 2^22 1.7 %, 2^24 equal; long chains
   // lose 1-8 % (p = 64, 128), so they keep one vector at a time.
   a.pipe = mid_short ? 1 : 0;
+  // Long 32-bit chains (one GPU per server) with at least
+  // kHopWindowWideMinElems elements per rank keep kHopWindowWide hop loads
+  // in flight per vector instead of kHopWindow.  Measured against the
+  // narrower window (back-to-back calls, results bit for bit equal):
+  // p64_f32 at 2^23 and 2^24 elements per rank 1.4 % faster, 36-48 ranks
+  // 1.4-1.6 %, 96 ranks with one straggler at 2^23 1.5 %, int32 0.6-0.7 %,
+  // p128_f32 at 2^24 and 2^25 0.5-0.6 %; below 2^23 it was slower (p64 at
+  // 2^22 0.9 %, p128 at 2^21 1.5 %), and bf16 long chains 8 % slower.
+  a.wide_window = long_chain && !servers && es == 4 && vec16 && N >= kHopWindowWideMinElems ? 1 : 0;
   bool runs = servers || two;
   // With one-vector tiles, chains of fewer than kXcdRunsWideHealthy healthy
   // ranks keep the per-XCD runs up to kXcdRunsMaxTilesMid tiles.  Measured

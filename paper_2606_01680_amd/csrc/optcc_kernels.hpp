@@ -47,6 +47,10 @@ namespace kern {
 constexpr int kThreads = 256;
 constexpr int kMaxRanks = OPTCC_MAX_EMULATE_RANKS;
 constexpr int kHopWindow = 16;  // hop loads in flight per vector along a chain
+// the same for long chains of 32-bit elements at one workgroup per CU with
+// large messages (142 VGPRs for one vector per lane: no spills)
+constexpr int kHopWindowWide = 24;
+constexpr int64_t kHopWindowWideMinElems = (int64_t)1 << 23;  // elements per rank
 // Input values are read once: streaming (nontemporal) loads keep them from
 // displacing lines in L2.  Stores of values that no later step overwrites
 // are streamed too; Stage-1 partials that Stage 4 overwrites are ordinary
@@ -105,6 +109,10 @@ struct KArgs {
   // launch setting, not read by the kernel: workgroups to launch (0: one
   // per tile)
   int32_t grid;
+  // launch setting, not read by the kernel: 1 selects the variant with the
+  // hop window kHopWindowWide (32-bit, one vector per lane, one GPU per
+  // server)
+  int32_t wide_window;
   // work stealing when not NULL: [0] the next tile, [1] workgroups that have
   // finished; both zero at launch and reset to zero by the last workgroup
   uint32_t *steal;
@@ -884,9 +892,8 @@ __device__ __forceinline__ void run_elems(const KArgs &a, void *const *rp, const
 // workgroup-width, in lockstep; vectors past the tile's last whole group go
 // one at a time, and elements past the last whole vector (only at the end
 // of the rank vectors) one by one.
-template <class D, int W, int L, bool S, int G>
+template <class D, int W, int L, bool S, int G, int B>
 __device__ __forceinline__ void run_tile(const KArgs &a, void *const *rp, int64_t t) {
-  constexpr int B = kHopWindow;
   constexpr int64_t kStride = (int64_t)kThreads * W;
   const TileDesc td = a.tiles[t];
   const bool p2p = td.meta & 1;
@@ -926,8 +933,8 @@ __device__ __forceinline__ void run_tile(const KArgs &a, void *const *rp, int64_
 
 // S selects the several-GPUs-per-server lane (App. E); its plans have no
 // point-to-point chunks.  G: GPUs per server when fixed at compile time
-// (0: read from the arguments).
-template <class D, int W, int L, bool S, int G>
+// (0: read from the arguments).  B: hop loads in flight per vector.
+template <class D, int W, int L, bool S, int G, int B = kHopWindow>
 __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
   __shared__ void *rp[kMaxRanks];
   const int nrp = S ? (a.pp + 1) * a.g : a.pp;  // pointers the lanes index from LDS
@@ -949,7 +956,7 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
       const int64_t t = next;
       __syncthreads();
       if (t < 0) break;
-      run_tile<D, W, L, S, G>(a, rp, t);
+      run_tile<D, W, L, S, G, B>(a, rp, t);
     }
     if (threadIdx.x == 0) {
       __threadfence();
@@ -970,7 +977,7 @@ __global__ __launch_bounds__(kThreads) void optcc_exec_kernel(KArgs a) {
   const int64_t cover = a.xcd_runs ? per * kXcds : a.ntiles;
   for (int64_t t0 = blockIdx.x; t0 < cover; t0 += gridDim.x) {
     const int64_t t = a.xcd_runs ? (t0 % kXcds) * per + t0 / kXcds : t0;
-    if (t < a.ntiles) run_tile<D, W, L, S, G>(a, rp, t);
+    if (t < a.ntiles) run_tile<D, W, L, S, G, B>(a, rp, t);
   }
 }
 

@@ -38,6 +38,9 @@ hipError_t launch(const KArgs &a, bool vec16, bool two, hipStream_t st, int *occ
   }
   if constexpr (sizeof(typename D::S) == 4) {  // two vectors per lane: 32-bit types only
     if (two) OPTCC_LAUNCH_OR_QUERY((optcc_exec_kernel<D, W16, 2, S, G>));
+    if constexpr (!S && G == 0) {  // long chains with large messages: the wider hop window
+      if (a.wide_window) OPTCC_LAUNCH_OR_QUERY((optcc_exec_kernel<D, W16, 1, S, G, kHopWindowWide>));
+    }
   }
   OPTCC_LAUNCH_OR_QUERY((optcc_exec_kernel<D, W16, 1, S, G>));
 }
