@@ -924,6 +924,42 @@ def test_three_workgroups_per_cu_edges(o, case):
     torch.cuda.empty_cache()
 
 
+WIDE_WINDOW_CASES = [
+    # 32-bit chains of more than 32 healthy ranks keep 24 hop loads in flight
+    # from 2^23 elements per rank (16-byte-aligned buffers); just below, with
+    # element-aligned buffers and for bf16 they keep 16
+    ("p=34 at 0.5, fp32, 2^23 (24 loads)", 34, {33: 0.5}, 1 << 23, "f32"),
+    ("p=34 at 0.5, int32, 2^23 - 4 (16 loads)", 34, {33: 0.5}, (1 << 23) - 4, "i32"),
+    ("p=40, two stragglers, int32, 2^23 + 4 (24 loads)", 40, {38: 0.5, 39: 0.75},
+     (1 << 23) + 4, "i32"),
+    ("p=34 at 0.5, fp32, odd N (one element per access)", 34, {33: 0.5}, (1 << 23) + 1, "f32"),
+    ("p=64 at 0.875 (P2P chunks), fp32, 2^23 (24 loads)", 64, {63: 0.875}, 1 << 23, "f32"),
+    ("p=34 at 0.5, bf16, 2^23 (16 loads)", 34, {33: 0.5}, 1 << 23, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", WIDE_WINDOW_CASES, ids=[c[0] for c in WIDE_WINDOW_CASES])
+def test_wide_hop_window_edges(o, case):
+    """Long chains on both sides of the launch rule that selects the kernel
+    with the deeper hop-load window (32-bit elements, at least 2^23 per
+    rank, 16-byte-aligned buffers): every element of every rank bit for bit
+    against the oracle's full serial run."""
+    label, p, strag, n, dtype = case
+    _say(f"case wide hop window edge: {label}: p={p} n={n} dtype={dtype}")
+    bw = _bw(p, strag)
+    pl = o.optcc_plan(p, bw, n, 64)
+    x = rand_inputs(dtype, p, n, 2424 + p)
+    d = to_device(x, dtype)
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    got = to_host(d, dtype)
+    del d
+    ref = oracle.run(oracle.Schedule(p, bw, n, 64), dtype, x)
+    assert bits_equal(got, ref), label
+    del x, got, ref
+    torch.cuda.empty_cache()
+
+
 def test_random_large_short_chains(o):
     """Four seeded random plans of 6-8 healthy ranks with 480 MiB to 1.9 GiB
     of rank buffers (the range where 6-7 healthy ranks launch at three
