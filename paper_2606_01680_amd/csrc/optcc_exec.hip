@@ -459,6 +459,19 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     const int resident = resident_workgroups(a, dtype, servers, vec16, two_vec);
     runs = resident <= 0 || ntiles > resident;
   }
+  // Server plans of at least kXcdRunsWideHealthy ranks (one workgroup per
+  // CU) with more than kServerStealMinTiles tiles take work stealing (below)
+  // instead of the per-XCD runs, when it is available; otherwise the runs.
+  // Measured (back-to-back calls, results bit for bit equal) at 2^24
+  // elements per rank (8192 tiles): 32 x 4 fp32 0.8 %, int32 1.1 %, bf16
+  // 7.6 % faster, 64 x 2 3.2 %, 16 x 8 4.2 %, 24 x 4 4.9 % (0.6 % slower
+  // on another GPU); 32 x 4 fp32 at 2^25 0.4 % slower.  At 4096 tiles it was mixed (32 x 4 fp32 3.7 % and
+  // 48 x 4 4.6 % faster, 24 x 4 6.5 % slower), at 2048 tiles and below
+  // 5-10 % slower, and 64-rank server plans at 8192 tiles 2.7 % slower
+  // (fp32, int32; bf16 2.5 % faster).
+  const bool server_steal = servers && long_chain && vec16 && pl->p >= kXcdRunsWideHealthy &&
+                            ntiles > kServerStealMinTiles && !noalloc;
+  if (server_steal) runs = false;
   a.xcd_runs = runs ? 1 : 0;
   // Work stealing for the same long chains at one workgroup per CU when
   // their tiles take the identity order (more than runs_max): a
@@ -475,7 +488,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // launch keeps its counter block, and replays of the graph on two streams
   // at once would share it; the no-allocation entry point keeps the static
   // order too.
-  bool steal = long_chain && !servers && a.occ_lds > 0 && !runs && !noalloc;
+  bool steal = long_chain && (!servers || server_steal) && a.occ_lds > 0 && !runs && !noalloc;
   int steal_grid = 0;
   if (steal) {
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -485,6 +498,7 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     steal_grid = resident_workgroups(a, dtype, servers, vec16, two_vec);
     steal = steal_grid > 0 && steal_grid < ntiles;
   }
+  if (server_steal && !steal) a.xcd_runs = 1;  // captured: the server plans' runs
   DeviceTables dt;
   int rc = noalloc ? scratch_tables(*pl, tile_elems, st, &dt)
                    : device_tables(*pl, tile_elems, st, &dt);

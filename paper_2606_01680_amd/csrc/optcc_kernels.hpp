@@ -69,6 +69,9 @@ constexpr int kTwoVectorMaxHealthy = 32;
 constexpr int64_t kXcdRunsMaxTiles = 2048;
 constexpr int64_t kXcdRunsMaxTilesMid = 4096;
 constexpr int kXcdRunsWideHealthy = 90;
+// server plans of at least kXcdRunsWideHealthy ranks take work stealing
+// above this many tiles
+constexpr int64_t kServerStealMinTiles = 4096;
 // mid-size messages on one-GPU-per-server chains of 32-bit elements with at
 // most this many healthy ranks, whose rank buffers total at least
 // kOneVectorMinBytes and less than kOneVectorMaxBytes, run one vector per

@@ -343,3 +343,44 @@ def test_server_largest_rank_count(o, q, g):
         _say(f"case servers p=256 q={q} g={g} dtype={dtype}")
         x, ref, got = _run_both(o, q, g, slow, 20000, 24, dtype, seed=q * 7 + g)
         assert bits_equal(got, ref)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype,q,g,slow,n", [
+    # 90 or more ranks, more than 4096 tiles, 16-byte-aligned buffers: work
+    # stealing; fewer tiles, element-aligned buffers or fewer ranks: the
+    # per-XCD runs
+    ("bf16", 24, 4, {23: 0.5}, (1 << 23) + (1 << 20) + 8),
+    ("bf16", 32, 4, {5: 0.875}, (1 << 23) + (1 << 21) + 16),
+    ("f32", 45, 2, {44: 0.5}, (1 << 23) + 2048 * 3 + 4),
+    ("bf16", 24, 4, {23: 0.5}, 1 << 22),
+    ("bf16", 24, 4, {23: 0.5}, (1 << 23) + (1 << 20) + 1),
+    ("bf16", 22, 4, {21: 0.5}, (1 << 23) + (1 << 20) + 8),
+])
+def test_server_work_stealing(o, dtype, q, g, slow, n):
+    """Server plans on both sides of the work-stealing rule (90 or more
+    ranks, more than 4096 tiles of 2048 elements, 16-byte-aligned buffers):
+    three calls on one plan, the first two from the same inputs (the device
+    counter block of the first is reset for the second), the third on the
+    second's output, each bit for bit against the oracle on every
+    element."""
+    torch = _gpu()
+    from gpu_util import bits_equal, rand_inputs, to_device, to_host
+    _say(f"case servers work stealing dtype={dtype} q={q} g={g} slow={slow} n={n}")
+    bw = _sbw(q, slow)
+    k = 64
+    x = rand_inputs(dtype, q * g, n, q * 31 + g, "normal")
+    ref = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy())
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    for call in range(2):
+        d = to_device(x, dtype)
+        o.optcc_allreduce_emulate(d, q * g, n, dtype, pl)
+        torch.cuda.synchronize()
+        got = to_host(d, dtype)
+        assert bits_equal(got, ref), f"call {call}"
+    ref2 = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, ref.copy())
+    o.optcc_allreduce_emulate(d, q * g, n, dtype, pl)
+    torch.cuda.synchronize()
+    assert bits_equal(to_host(d, dtype), ref2), "call 2"
+    del d
+    torch.cuda.empty_cache()
