@@ -313,9 +313,9 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
   // Launch shape.  Short chains (inputs per lane: P' for one GPU per
   // server, p for several): two vectors per lane (measured faster up to 32
   // and neutral or slower beyond).  Longer chains run one workgroup per CU.
-  // Per-XCD tile runs: for short chains, for every server plan (beyond 32
+  // Per-XCD tile runs: for short chains, for server plans (beyond 32
   // ranks, together with one workgroup per CU, 2.4-27 % faster than with
-  // neither) and for longer one-GPU-per-server chains whose tiles are more
+  // neither; the largest take work stealing instead, below) and for longer one-GPU-per-server chains whose tiles are more
   // than one round of resident workgroups and at most kXcdRunsMaxTiles
   // (measured with 2048-element tiles, p = 64 and 128 at 2^19-2^22 elements
   // per rank: 2.4-14 % faster; at 4096 tiles -8 % at p = 64, +4 % at
