@@ -332,6 +332,49 @@ def test_server_graph_capture_replays(o):
 
 
 @pytest.mark.gpu
+def test_server_graph_capture_of_a_stealing_plan(o):
+    """A server plan whose eager launches take work stealing (96 ranks, more
+    than 4096 tiles) keeps the per-XCD runs when captured in a HIP graph:
+    every replay equals the eager result and the oracle bit for bit."""
+    torch = _gpu()
+    from gpu_util import bits_equal, rand_inputs, to_device, to_host
+    q, g, n, k, dtype = 24, 4, (1 << 23) + (1 << 20) + 8, 64, "bf16"
+    bw = _sbw(q, {23: 0.5})
+    p = q * g
+    pl = o.optcc_plan_servers(q, g, bw, n, k)
+    x = rand_inputs(dtype, p, n, 43)
+    d = to_device(x, dtype)
+    d0 = d.clone()
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    eager = d.clone()
+    ref = oracle.run(oracle.Schedule.servers(q, g, bw, n, k), dtype, x.copy())
+    assert bits_equal(to_host(eager, dtype), ref)
+    gr = torch.cuda.CUDAGraph()
+    d.copy_(d0)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(gr, stream=s):
+            o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    for rep in range(2):
+        _say(f"case server graph replay of a stealing plan rep={rep}")
+        d.copy_(d0)
+        torch.cuda.synchronize()
+        gr.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(d.view(torch.int16), eager.view(torch.int16))
+    # eager again after the capture: stealing, same bits
+    d.copy_(d0)
+    o.optcc_allreduce_emulate(d, p, n, dtype, pl)
+    torch.cuda.synchronize()
+    assert torch.equal(d.view(torch.int16), eager.view(torch.int16))
+    del gr, d, d0, eager
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.gpu
 @pytest.mark.parametrize("q,g", [(32, 8), (4, 64), (128, 2)])
 def test_server_largest_rank_count(o, q, g):
     """p = q g = 256 ranks, the executor's limit: 32 servers x 8 GPUs and
