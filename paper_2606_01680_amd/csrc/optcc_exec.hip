@@ -460,17 +460,21 @@ int emulate(void *const *bufs, int p, int64_t N, optcc_dtype_t dtype, const optc
     runs = resident <= 0 || ntiles > resident;
   }
   // Server plans of at least kXcdRunsWideHealthy ranks (one workgroup per
-  // CU) with more than kServerStealMinTiles tiles take work stealing (below)
-  // instead of the per-XCD runs, when it is available; otherwise the runs.
-  // Measured (back-to-back calls, results bit for bit equal) at 2^24
-  // elements per rank (8192 tiles): 32 x 4 fp32 0.8 %, int32 1.1 %, bf16
-  // 7.6 % faster, 64 x 2 3.2 %, 16 x 8 4.2 %, 24 x 4 4.9 % (0.6 % slower
-  // on another GPU); 32 x 4 fp32 at 2^25 0.4 % slower.  At 4096 tiles it was mixed (32 x 4 fp32 3.7 % and
-  // 48 x 4 4.6 % faster, 24 x 4 6.5 % slower), at 2048 tiles and below
-  // 5-10 % slower, and 64-rank server plans at 8192 tiles 2.7 % slower
+  // CU) with more than kServerStealMinTiles tiles (kXcdRunsMaxTiles from
+  // kServerStealWideRanks ranks) take work stealing (below) instead of the
+  // per-XCD runs, when it is available; otherwise the runs.  Measured
+  // (back-to-back calls, results bit for bit equal) at 2^24 elements per
+  // rank (8192 tiles): 32 x 4 fp32 0.8 %, int32 1.1 %, bf16 7.6 % faster,
+  // 64 x 2 3.2 %, 16 x 8 4.2 %, 24 x 4 4.9 % (0.6 % slower on another
+  // GPU); 32 x 4 fp32 at 2^25 0.4 % slower.  At 4096 tiles: 128 ranks and
+  // more faster (32 x 4 fp32 3.7-4.3 %, bf16 2.6 %, 64 x 2 0.2 %, 30 x 4 3.2 %, 48 x 4
+  // 4.6 %), 24 x 4 6.5 % slower; at 2048 tiles and below 5-10 % slower
+  // (48 x 4 0.9 % faster); 64-rank server plans at 8192 tiles 2.7 % slower
   // (fp32, int32; bf16 2.5 % faster).
+  const int64_t server_steal_min =
+      pl->p >= kServerStealWideRanks ? kXcdRunsMaxTiles : kServerStealMinTiles;
   const bool server_steal = servers && long_chain && vec16 && pl->p >= kXcdRunsWideHealthy &&
-                            ntiles > kServerStealMinTiles && !noalloc;
+                            ntiles > server_steal_min && !noalloc;
   if (server_steal) runs = false;
   a.xcd_runs = runs ? 1 : 0;
   // Work stealing for the same long chains at one workgroup per CU when

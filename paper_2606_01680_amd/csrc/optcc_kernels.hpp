@@ -72,6 +72,8 @@ constexpr int kXcdRunsWideHealthy = 90;
 // server plans of at least kXcdRunsWideHealthy ranks take work stealing
 // above this many tiles
 constexpr int64_t kServerStealMinTiles = 4096;
+// ... and above kXcdRunsMaxTiles tiles from this many ranks
+constexpr int kServerStealWideRanks = 120;
 // mid-size messages on one-GPU-per-server chains of 32-bit elements with at
 // most this many healthy ranks, whose rank buffers total at least
 // kOneVectorMinBytes and less than kOneVectorMaxBytes, run one vector per

@@ -390,19 +390,25 @@ def test_server_largest_rank_count(o, q, g):
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("dtype,q,g,slow,n", [
-    # 90 or more ranks, more than 4096 tiles, 16-byte-aligned buffers: work
-    # stealing; fewer tiles, element-aligned buffers or fewer ranks: the
-    # per-XCD runs
+    # 90 or more ranks, more than 4096 tiles (2048 from 120 ranks),
+    # 16-byte-aligned buffers: work stealing; fewer tiles, element-aligned
+    # buffers or fewer ranks: the per-XCD runs
     ("bf16", 24, 4, {23: 0.5}, (1 << 23) + (1 << 20) + 8),
     ("bf16", 32, 4, {5: 0.875}, (1 << 23) + (1 << 21) + 16),
     ("f32", 45, 2, {44: 0.5}, (1 << 23) + 2048 * 3 + 4),
     ("bf16", 24, 4, {23: 0.5}, 1 << 22),
     ("bf16", 24, 4, {23: 0.5}, (1 << 23) + (1 << 20) + 1),
     ("bf16", 22, 4, {21: 0.5}, (1 << 23) + (1 << 20) + 8),
+    # from 120 ranks the bound is 2048 tiles
+    ("f32", 32, 4, {31: 0.875}, (1 << 22) + (1 << 20) + 4),
+    ("bf16", 30, 4, {29: 0.5}, (1 << 22) + (1 << 20) + 8),
+    ("bf16", 29, 4, {28: 0.5}, (1 << 22) + (1 << 20) + 8),
+    ("bf16", 32, 4, {31: 0.5}, 1 << 21),
 ])
 def test_server_work_stealing(o, dtype, q, g, slow, n):
     """Server plans on both sides of the work-stealing rule (90 or more
-    ranks, more than 4096 tiles of 2048 elements, 16-byte-aligned buffers):
+    ranks, more than 4096 tiles of 2048 elements, more than 2048 from 120
+    ranks, 16-byte-aligned buffers):
     three calls on one plan, the first two from the same inputs (the device
     counter block of the first is reset for the second), the third on the
     second's output, each bit for bit against the oracle on every
