@@ -161,7 +161,8 @@ void optcc_plan_free(optcc_plan_t *plan);
  * (4,096 with fewer than 90 healthy ranks; a tile is one 16-byte vector per
  * lane, 1,024 elements for 32-bit types, for these plans), and plans of 90
  * or more ranks with several GPUs per server whose tiles (2,048 elements
- * here) outnumber 4,096 and whose buffers are 16-byte aligned,
+ * here) outnumber 4,096 (2,048 from 120 ranks) and whose buffers are
+ * 16-byte aligned,
  * run a grid of the resident workgroups that take tiles from a device
  * counter.  Each such call takes its own 64-byte counter block from a ring
  * of 4,096 per plan and device (256 KiB, allocated and zeroed by the plan's
